@@ -1,0 +1,260 @@
+#!/usr/bin/env python3
+"""Benchmark of the W4A16 GEMM on one MI355X.
+
+One step = the whole hot path over the workload: every decoder-linear GEMM of
+the Llama-2-7B set (4 shapes x M in {1,4,16,64,128,256}) and of the
+Llama-2-70B set (4 shapes x M in {1,16,128,512,1024}), 44 GEMMs, each with
+its own device copy of the packed weights (2.7 GB in all, far beyond the
+256 MB Infinity Cache, so every launch streams its weights from HBM).  Inputs
+are seeded synthetic tensors from workloads.py, resident in HBM before the
+timed region.  The offline pack runs once, untimed, before it.
+
+Printed: one JSON line with the aggregate TFLOP/s (value), the HBM GB/s,
+the roofline of the dominant kernel measured with HIP events on the launch
+stream, a second roofline for the bandwidth-bound small-M points, and the
+CPU oracle's rate on a bounded sample (cpu_baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, GB/s
+MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak, TFLOP/s
+METRIC = "W4A16 GEMM TFLOPS + HBM GB/s vs roofline, M=1..1024, Llama-7B/70B shapes"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_name(sel: dict) -> str:
+    if sel["variant"] == 1:
+        return "stream_kernel<MT,%d,%d>" % (sel["tile_n"], sel["split_k"])
+    name = "tiled_kernel<%d,%d>" % (sel["tile_m"], sel["tile_n"])
+    if sel["split_k"] > 1:
+        name += "+splitk_reduce(S=%d)" % sel["split_k"]
+    return name
+
+
+def build_points(configs):
+    import workloads as W
+    pts = []
+    for cid in configs:
+        cfg = W.CONFIGS[cid]
+        for si, sh in enumerate(cfg.shapes):
+            for M in sh.Ms:
+                pts.append(dict(cid=cid, si=si, shape=sh.name, K=sh.K, N=sh.N, M=M))
+    return pts
+
+
+def cpu_baseline(points, threads: int, col_fraction: float):
+    """The oracle (as it stands) on a bounded sample: every (shape, M) point,
+    all rows, a seeded sample of ceil(N * col_fraction) columns."""
+    import oracle
+    import workloads as W
+    t_total = 0.0
+    fl_total = 0
+    cache = {}
+    for p in points:
+        key = (p["cid"], p["si"])
+        if key not in cache:
+            cache.clear()
+            cfg = W.CONFIGS[p["cid"]]
+            sh = cfg.shapes[p["si"]]
+            x = W.draw_x(p["cid"], p["si"], max(sh.Ms), sh.K, cfg.outliers)
+            cache[key] = (x,) + W.draw_weights(p["cid"], p["si"], sh.K, sh.N)
+        x, q, z, s = cache[key]
+        ncols = max(1, int(np.ceil(p["N"] * col_fraction)))
+        cols = W.sample_columns(p["N"], ncols, seed=1)
+        t0 = time.perf_counter()
+        oracle.gemm(x[:p["M"]], q, z, s, cols=cols, threads=threads)
+        t_total += time.perf_counter() - t0
+        fl_total += 2 * p["M"] * len(cols) * p["K"]
+    return fl_total, t_total
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--configs", default="2,5", help="workload configs (2 = Llama-2-7B, 5 = Llama-2-70B)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-col-fraction", type=float, default=1.0 / 32)
+    ap.add_argument("--points-out", default="", help="optional path for the per-GEMM table (JSON)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures the single-GPU path only: this build runs on one MI355X "
+              "(--gpus 1); multi-GPU runs are not part of it.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2402_10076_amd as Q
+    import workloads as W
+
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    Q.lib()  # raises if the HIP library is not built
+
+    configs = [int(c) for c in args.configs.split(",") if c]
+    points = build_points(configs)
+    dev = torch.device("cuda:0")
+
+    # ---- inputs: generate, pack (untimed, host), upload one weight copy per point
+    t_setup = time.perf_counter()
+    xs = {}
+    for p in points:
+        key = (p["cid"], p["si"])
+        if key not in xs:
+            cfg = W.CONFIGS[p["cid"]]
+            sh = cfg.shapes[p["si"]]
+            log("setup C%d %s K=%d N=%d" % (p["cid"], sh.name, sh.K, sh.N))
+            q, z, s = W.draw_weights(p["cid"], p["si"], sh.K, sh.N)
+            pw, ps, pz = Q.pack_weights(q, z, s)
+            del q, z, s
+            base = Q.to_device(pw, ps, pz, dev)
+            del pw, ps, pz
+            x = W.draw_x(p["cid"], p["si"], max(sh.Ms), sh.K, cfg.outliers)
+            xd = torch.from_numpy(x.view(np.int16)).to(dev).view(torch.float16)
+            xs[key] = (xd, base)
+        xd, base = xs[key]
+        p["w"] = tuple(t.clone() for t in base)
+        p["x"] = xd[:p["M"]]
+        p["y"] = torch.empty((p["M"], p["N"]), dtype=torch.float16, device=dev)
+        p["sel"] = Q.select_config(p["M"], p["N"], p["K"])
+        p["kernel"] = kernel_name(p["sel"])
+        p["flops"] = W.flops(p["M"], p["N"], p["K"])
+        p["bytes"] = W.alg_bytes(p["M"], p["N"], p["K"])
+    xs.clear()
+    torch.cuda.synchronize()
+    log("setup %.1f s, %d GEMMs per step, %.2f GB of packed weights on device" % (
+        time.perf_counter() - t_setup, len(points),
+        sum(sum(t.numel() * t.element_size() for t in p["w"]) for p in points) / 1e9))
+
+    def step(evs=None):
+        for i, p in enumerate(points):
+            if evs is not None:
+                evs[i][0].record()
+            Q.w4a16_gemm(p["x"], *p["w"], p["N"], y=p["y"])
+            if evs is not None:
+                evs[i][1].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in points] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(evs[s])
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+
+    for i, p in enumerate(points):
+        p["ms"] = float(np.mean([evs[s][i][0].elapsed_time(evs[s][i][1]) for s in range(args.steps)]))
+        p["tflops"] = p["flops"] / (p["ms"] * 1e-3) / 1e12
+        p["gbs"] = p["bytes"] / (p["ms"] * 1e-3) / 1e9
+        p["frac_hbm"] = p["gbs"] / HBM_PEAK_GBS
+        p["frac_mfma"] = p["tflops"] / MFMA_F16_PEAK_TFLOPS
+        p["bound"] = "hbm" if p["bytes"] / HBM_PEAK_GBS >= p["flops"] / 1e3 / MFMA_F16_PEAK_TFLOPS else "mfma"
+        p["frac_roof"] = p["frac_hbm"] if p["bound"] == "hbm" else p["frac_mfma"]
+
+    log("%-4s %-8s %6s %6s %6s %-34s %9s %8s %8s %6s %6s" % (
+        "cfg", "shape", "K", "N", "M", "kernel", "us", "TFLOP/s", "GB/s", "fHBM", "fMFMA"))
+    for p in points:
+        log("C%-3d %-8s %6d %6d %6d %-34s %9.2f %8.1f %8.0f %6.3f %6.3f" % (
+            p["cid"], p["shape"], p["K"], p["N"], p["M"], p["kernel"], p["ms"] * 1e3, p["tflops"],
+            p["gbs"], p["frac_hbm"], p["frac_mfma"]))
+
+    tot_flops = sum(p["flops"] for p in points)
+    tot_bytes = sum(p["bytes"] for p in points)
+    ms_per_step = elapsed / args.steps * 1e3
+
+    # dominant kernel: the kernel (by name) with the most event time per step
+    by_k = {}
+    for p in points:
+        by_k.setdefault(p["kernel"], []).append(p)
+    dom = max(by_k, key=lambda k: sum(p["ms"] for p in by_k[k]))
+    dpts = by_k[dom]
+    d_ms = sum(p["ms"] for p in dpts)
+    d_bound = "mfma" if all(p["bound"] == "mfma" for p in dpts) else "hbm"
+    if d_bound == "mfma":
+        ach = sum(p["flops"] for p in dpts) / (d_ms * 1e-3) / 1e12
+        roof = dict(bound="mfma", achieved=round(ach, 2), peak=MFMA_F16_PEAK_TFLOPS, unit="TFLOP/s",
+                    frac=round(ach / MFMA_F16_PEAK_TFLOPS, 4), traffic=None)
+    else:
+        ach = sum(p["bytes"] for p in dpts) / (d_ms * 1e-3) / 1e9
+        roof = dict(bound="hbm", achieved=round(ach, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                    frac=round(ach / HBM_PEAK_GBS, 4), traffic=None)
+    roof["kernel"] = dom
+    roof["launches_per_step"] = len(dpts)
+    roof["avg_launch_us"] = round(d_ms * 1e3 / len(dpts), 2)
+
+    small = [p for p in points if p["M"] <= 16]
+    s_ms = sum(p["ms"] for p in small)
+    s_gbs = sum(p["bytes"] for p in small) / (s_ms * 1e-3) / 1e9 if small else 0.0
+    big = [p for p in points if p["M"] >= 256]
+    b_ms = sum(p["ms"] for p in big)
+    b_tf = sum(p["flops"] for p in big) / (b_ms * 1e-3) / 1e12 if big else 0.0
+
+    out = {
+        "metric": METRIC,
+        "value": round(tot_flops * args.steps / elapsed / 1e12, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {
+            "workload": "W4A16 g128 decoder-linear GEMMs: Llama-2-7B (K,N) in {(4096,12288),(4096,4096),"
+                        "(4096,22016),(11008,4096)} x M in {1,4,16,64,128,256} and Llama-2-70B "
+                        "{(8192,10240),(8192,8192),(8192,57344),(28672,8192)} x M in {1,16,128,512,1024}",
+            "gemms_per_step": len(points),
+            "group": 128,
+            "weights": "uint4 q, uint4 zero, fp16 scale per 128 input channels; one packed copy per GEMM",
+        },
+        "hbm_gbps": round(tot_bytes * args.steps / elapsed / 1e9, 1),
+        "roofline": roof,
+        "roofline_small_m": dict(bound="hbm", achieved=round(s_gbs, 1), peak=HBM_PEAK_GBS, unit="GB/s",
+                                 frac=round(s_gbs / HBM_PEAK_GBS, 4), points=len(small),
+                                 scope="all GEMMs with M<=16, event-timed"),
+        "mfma_large_m": dict(achieved=round(b_tf, 2), peak=MFMA_F16_PEAK_TFLOPS, unit="TFLOP/s",
+                             frac=round(b_tf / MFMA_F16_PEAK_TFLOPS, 4), points=len(big),
+                             scope="all GEMMs with M>=256, event-timed"),
+    }
+
+    if not args.no_cpu_baseline:
+        threads = min(16, len(os.sched_getaffinity(0)))
+        log("cpu baseline: oracle on %d threads, %.4f of the columns of every GEMM" % (
+            threads, args.cpu_col_fraction))
+        fl, t = cpu_baseline(points, threads, args.cpu_col_fraction)
+        out["cpu_baseline"] = {
+            "value": round(fl / t / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": "every GEMM of the step, all rows, a seeded sample of ceil(N/%d) columns "
+                      "(%.1f GFLOP in %.1f s)" % (round(1 / args.cpu_col_fraction), fl / 1e9, t),
+        }
+
+    if args.points_out:
+        with open(args.points_out, "w") as f:
+            json.dump([{k: v for k, v in p.items() if k not in ("w", "x", "y")} for p in points], f, indent=1)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,142 @@
+/*
+ * quick.h -- C ABI of the MI355X (gfx950) W4A16 mixed-precision GEMM library.
+ *
+ * The operation (paper, Section 2.1 and Section 2.3): weights are stored as
+ * 4-bit unsigned integers q with one zero point z (4-bit) and one scale s
+ * (binary16) per group of 128 consecutive input channels of an output
+ * column; they are dequantized to W = (q - z) * s and multiplied by binary16
+ * activations x, y = x . W.  Following Section 3.1 and Section 3.2 the static
+ * weights are reordered once, offline (quick_pack_weights), so that the GEMM
+ * kernels load them from memory straight into the registers of the gfx950
+ * matrix-instruction operand and dequantize them there, without ever writing
+ * dequantized weights to shared memory (LDS).
+ *
+ * Conventions shared by every entry point:
+ *  - Every function returns a quick status code (QUICK_OK == 0) and never
+ *    throws.  All validation happens before any write or launch: on an error
+ *    nothing has been written and nothing has been enqueued.
+ *  - Every buffer is owned by the caller.  The library keeps no pointer to a
+ *    caller buffer after the call returns.
+ *  - Matrices are dense and row-major.  "f16" means IEEE binary16 bit
+ *    patterns stored in uint16_t.
+ *  - Only group == 128 is supported (QUICK_ERR_UNSUPPORTED otherwise);
+ *    K must be a multiple of 128 and N a multiple of 16 (QUICK_ERR_SHAPE).
+ */
+#ifndef QUICK_H
+#define QUICK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ---------------------------------------------------- */
+#define QUICK_OK 0
+#define QUICK_ERR_INVALID_ARG 1  /* null pointer, bad config field          */
+#define QUICK_ERR_SHAPE 2        /* M < 0, K % 128, N % 16, K or N <= 0     */
+#define QUICK_ERR_UNSUPPORTED 3  /* group != 128                             */
+#define QUICK_ERR_RANGE 4        /* a q or z value above 15                  */
+#define QUICK_ERR_ALIGNMENT 5    /* device pointer not aligned (see below)   */
+#define QUICK_ERR_HIP 6          /* HIP runtime error (launch, allocation)   */
+#define QUICK_ERR_WORKSPACE 7    /* caller workspace missing or too small    */
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* quick_status_string(int status);
+
+/* Identifier of the packed weight layout produced by quick_pack_weights.
+ * 1 == "QPK16": units of 16 output columns x 128 input channels, 1 KiB of
+ * packed weights each, ordered for the 16x16x32 f16 matrix instruction. */
+int quick_pack_format_version(void);
+
+/* ---- offline packing (host memory, no device work, reentrant) --------- */
+
+/* Byte sizes of the three packed buffers for a K x N weight matrix:
+ * packed weights K*N/2, packed zero points K*N/256, packed scales K*N/64.
+ * Any output pointer may be NULL.  Errors: SHAPE, UNSUPPORTED. */
+int quick_packed_sizes(int64_t K, int64_t N, int64_t group,
+                       size_t* packed_bytes, size_t* zeros_bytes, size_t* scales_bytes);
+
+/* Offline reorder of the static quantized weights (Section 3.1, 3.2).
+ *   q      [K][N]          uint8, one 4-bit value (0..15) per byte
+ *   z      [K/group][N]    uint8, zero points 0..15
+ *   s      [K/group][N]    f16 scales
+ * Outputs (host memory, sizes from quick_packed_sizes, fully overwritten):
+ *   packed  QPK16 weights: for n-tile nt = n/16 and k-group kg = k/128 the
+ *           1 KiB unit ((nt*K/128 + kg)) holds 64 lanes x 4 words; lane
+ *           16*((k%32)/8) + n%16, word (k%128)/32, and inside the word the
+ *           element e = k%8 sits in nibble e/2 (even e) or 4 + e/2 (odd e),
+ *           so that masking the word and its 8-bit shift with 0x000F000F and
+ *           0x00F000F0 yields element pairs (0,1), (2,3), (4,5), (6,7).
+ *   zeros   uint32 word (nt*K/128 + kg)*2 + (n%16)/8 holds z in nibble n%8.
+ *   scales  f16 at (nt*K/128 + kg)*16 + n%16.
+ * Errors: INVALID_ARG (NULL), SHAPE, UNSUPPORTED, RANGE (value > 15; the
+ * outputs are then left untouched). */
+int quick_pack_weights(const uint8_t* q, const uint8_t* z, const uint16_t* s,
+                       int64_t K, int64_t N, int64_t group,
+                       void* packed, void* scales, void* zeros);
+
+/* Exact inverse of quick_pack_weights (host memory). */
+int quick_unpack_weights(const void* packed, const void* scales, const void* zeros,
+                         int64_t K, int64_t N, int64_t group,
+                         uint8_t* q, uint8_t* z, uint16_t* s);
+
+/* ---- the GEMM (device memory, asynchronous) --------------------------- */
+
+/* y[M][N] (f16) = x[M][K] (f16) . W, W the dequantized packed weights.
+ * Accumulation is fp32 throughout (also across split-K partials); the one
+ * final rounding to f16 is round-to-nearest-even.  Each weight is
+ * dequantized to f16 as (q - z) * s with an exact subtraction and a single
+ * rounding of the product.
+ *   x, packed      device pointers, 16-byte aligned
+ *   scales         device pointer, 2-byte aligned
+ *   zeros          device pointer, 4-byte aligned
+ *   y              device pointer, 8-byte aligned; must not overlap inputs
+ *   stream         hipStream_t passed as void*, NULL = default stream
+ * M == 0 is a valid no-op.  The call returns after enqueueing; results are
+ * visible after the stream is synchronized.  The library may use an internal
+ * device workspace (split-K partial sums), allocated on first need per
+ * (device, stream) and kept until process exit; a call that grows it
+ * synchronizes `stream` first.  Calls on one stream are ordered; calls on
+ * different streams use different workspaces.
+ * Errors: INVALID_ARG, SHAPE, UNSUPPORTED, ALIGNMENT, HIP. */
+int quick_w4a16_gemm(const void* x, const void* packed, const void* scales,
+                     const void* zeros, void* y, int64_t M, int64_t N, int64_t K,
+                     int64_t group, void* stream);
+
+/* Kernel selection for quick_w4a16_gemm_ex (tests, benchmarks, tuning).
+ * Zero in any field means "choose automatically". */
+typedef struct quick_config {
+    int variant;   /* 0 auto, 1 = stream kernel (small M), 2 = tiled kernel   */
+    int split_k;   /* number of K slices (tiled kernel: across workgroups;
+                      stream kernel: waves per workgroup), 0 = auto          */
+    int tile_m;    /* tiled kernel rows per workgroup: 64, 128 or 256         */
+    int tile_n;    /* tiled kernel columns per wave: 32 or 64
+                      stream kernel: n-tiles per wave: 1 or 2                 */
+} quick_config_t;
+
+/* Same contract as quick_w4a16_gemm with an explicit kernel choice.
+ * workspace/workspace_bytes: optional caller-owned device buffer for split-K
+ * partial sums (16-byte aligned); when NULL the internal workspace is used.
+ * Errors as quick_w4a16_gemm, plus INVALID_ARG for an unsupported config
+ * and WORKSPACE when the caller buffer is smaller than
+ * quick_workspace_bytes(). */
+int quick_w4a16_gemm_ex(const void* x, const void* packed, const void* scales,
+                        const void* zeros, void* y, int64_t M, int64_t N, int64_t K,
+                        int64_t group, void* stream, const quick_config_t* cfg,
+                        void* workspace, size_t workspace_bytes);
+
+/* Workspace bytes quick_w4a16_gemm_ex needs for this shape and config
+ * (cfg NULL = automatic choice); 0 when no workspace is used. */
+size_t quick_workspace_bytes(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg);
+
+/* The configuration the automatic heuristic picks for a shape (for logs and
+ * benchmarks).  Errors: INVALID_ARG (NULL cfg), SHAPE. */
+int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config_t* cfg);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* QUICK_H */

@@ -1,0 +1,215 @@
+"""Python binding of libquick.so, the gfx950 W4A16 GEMM library.
+
+Argument marshalling only: every step of the GEMM runs in the library's HIP
+kernels and the offline pack runs in its host C++ code.  PyTorch provides the
+device memory and the stream.  There is no fallback: if the library is not
+built, importing the binding's functions raises.
+
+Entry points mirror include/quick.h:
+
+* ``packed_sizes(K, N, group=128)``
+* ``pack_weights(q, z, s_bits, group=128)`` -> (packed, scales, zeros) numpy
+* ``unpack_weights(packed, scales, zeros, K, N, group=128)``
+* ``w4a16_gemm(x, packed, scales, zeros, N, y=None, group=128, ...)``
+* ``select_config(M, N, K)``, ``workspace_bytes(M, N, K, cfg=None)``
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+
+# torch first: its HIP runtime (soname libamdhip64.so.7) is then the one
+# libquick.so binds to, so the process has a single HIP runtime.
+import torch  # noqa: E402
+import numpy as np  # noqa: E402
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libquick.so")
+
+QUICK_OK = 0
+QUICK_ERR_INVALID_ARG = 1
+QUICK_ERR_SHAPE = 2
+QUICK_ERR_UNSUPPORTED = 3
+QUICK_ERR_RANGE = 4
+QUICK_ERR_ALIGNMENT = 5
+QUICK_ERR_HIP = 6
+QUICK_ERR_WORKSPACE = 7
+
+VARIANT_AUTO = 0
+VARIANT_STREAM = 1
+VARIANT_TILED = 2
+
+_lock = threading.Lock()
+_lib = None
+
+
+class QuickError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (what, status_string(status) if _lib else "?", status))
+
+
+class QuickConfig(ctypes.Structure):
+    _fields_ = [("variant", ctypes.c_int), ("split_k", ctypes.c_int),
+                ("tile_m", ctypes.c_int), ("tile_n", ctypes.c_int)]
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+def lib():
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise ImportError("libquick.so is not built (run __graft_entry__.build() or "
+                                  "python -m paper_2402_10076_amd.build)")
+            L = ctypes.CDLL(LIB_PATH)
+            P, I64, SZ, I = ctypes.c_void_p, ctypes.c_int64, ctypes.c_size_t, ctypes.c_int
+            L.quick_status_string.argtypes = [I]
+            L.quick_status_string.restype = ctypes.c_char_p
+            L.quick_pack_format_version.argtypes = []
+            L.quick_pack_format_version.restype = I
+            L.quick_packed_sizes.argtypes = [I64, I64, I64, ctypes.POINTER(SZ), ctypes.POINTER(SZ),
+                                             ctypes.POINTER(SZ)]
+            L.quick_packed_sizes.restype = I
+            L.quick_pack_weights.argtypes = [P, P, P, I64, I64, I64, P, P, P]
+            L.quick_pack_weights.restype = I
+            L.quick_unpack_weights.argtypes = [P, P, P, I64, I64, I64, P, P, P]
+            L.quick_unpack_weights.restype = I
+            L.quick_w4a16_gemm.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P]
+            L.quick_w4a16_gemm.restype = I
+            L.quick_w4a16_gemm_ex.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P,
+                                              ctypes.POINTER(QuickConfig), P, SZ]
+            L.quick_w4a16_gemm_ex.restype = I
+            L.quick_workspace_bytes.argtypes = [I64, I64, I64, ctypes.POINTER(QuickConfig)]
+            L.quick_workspace_bytes.restype = SZ
+            L.quick_select_config.argtypes = [I64, I64, I64, ctypes.POINTER(QuickConfig)]
+            L.quick_select_config.restype = I
+            _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().quick_status_string(int(status)).decode()
+
+
+def _check(st: int, what: str):
+    if st != QUICK_OK:
+        raise QuickError(st, what)
+
+
+def _np_ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def pack_format_version() -> int:
+    return lib().quick_pack_format_version()
+
+
+def packed_sizes(K: int, N: int, group: int = 128):
+    a, b, c = ctypes.c_size_t(), ctypes.c_size_t(), ctypes.c_size_t()
+    _check(lib().quick_packed_sizes(K, N, group, ctypes.byref(a), ctypes.byref(b), ctypes.byref(c)),
+           "quick_packed_sizes")
+    return a.value, b.value, c.value
+
+
+def pack_weights(q, z, s_bits, group: int = 128):
+    """Offline reorder on the host.  q [K][N] uint8, z [K/g][N] uint8, s_bits
+    [K/g][N] uint16 (binary16).  Returns numpy (packed u32, scales u16,
+    zeros u32)."""
+    q = np.ascontiguousarray(q, np.uint8)
+    z = np.ascontiguousarray(z, np.uint8)
+    s = np.ascontiguousarray(s_bits, np.uint16)
+    K, N = q.shape
+    if z.shape != (K // group, N) or s.shape != (K // group, N):
+        raise QuickError(QUICK_ERR_SHAPE, "pack_weights: z and s must be [K/group][N]")
+    wb, zb, sb = packed_sizes(K, N, group)
+    pw = np.empty(wb // 4, np.uint32)
+    ps = np.empty(sb // 2, np.uint16)
+    pz = np.empty(zb // 4, np.uint32)
+    _check(lib().quick_pack_weights(_np_ptr(q), _np_ptr(z), _np_ptr(s), K, N, group,
+                                    _np_ptr(pw), _np_ptr(ps), _np_ptr(pz)), "quick_pack_weights")
+    return pw, ps, pz
+
+
+def unpack_weights(packed, scales, zeros, K: int, N: int, group: int = 128):
+    pw = np.ascontiguousarray(packed, np.uint32)
+    ps = np.ascontiguousarray(scales, np.uint16)
+    pz = np.ascontiguousarray(zeros, np.uint32)
+    wb, zb, sb = packed_sizes(K, N, group)
+    if pw.nbytes != wb or ps.nbytes != sb or pz.nbytes != zb:
+        raise QuickError(QUICK_ERR_SHAPE, "unpack_weights: buffer sizes do not match K, N")
+    q = np.empty((K, N), np.uint8)
+    z = np.empty((K // group, N), np.uint8)
+    s = np.empty((K // group, N), np.uint16)
+    _check(lib().quick_unpack_weights(_np_ptr(pw), _np_ptr(ps), _np_ptr(pz), K, N, group,
+                                      _np_ptr(q), _np_ptr(z), _np_ptr(s)), "quick_unpack_weights")
+    return q, z, s
+
+
+def to_device(packed, scales, zeros, device="cuda"):
+    """Copy host packed buffers into device tensors (int32 / int16 / int32)."""
+    return (torch.from_numpy(np.ascontiguousarray(packed).view(np.int32)).to(device),
+            torch.from_numpy(np.ascontiguousarray(scales).view(np.int16)).to(device),
+            torch.from_numpy(np.ascontiguousarray(zeros).view(np.int32)).to(device))
+
+
+def make_config(variant=0, split_k=0, tile_m=0, tile_n=0) -> QuickConfig:
+    return QuickConfig(variant, split_k, tile_m, tile_n)
+
+
+def select_config(M: int, N: int, K: int) -> dict:
+    c = QuickConfig()
+    _check(lib().quick_select_config(M, N, K, ctypes.byref(c)), "quick_select_config")
+    return c.as_dict()
+
+
+def workspace_bytes(M: int, N: int, K: int, cfg: QuickConfig | None = None) -> int:
+    return int(lib().quick_workspace_bytes(M, N, K, ctypes.byref(cfg) if cfg is not None else None))
+
+
+def _dptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def w4a16_gemm(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor,
+               N: int, y: torch.Tensor | None = None, group: int = 128,
+               cfg: QuickConfig | None = None, workspace: torch.Tensor | None = None,
+               stream=None) -> torch.Tensor:
+    """y = x . W on the GPU.  x: [M][K] float16 (contiguous, on the device);
+    packed/scales/zeros: device tensors from ``to_device``.  Runs on torch's
+    current stream unless ``stream`` (a torch.cuda.Stream) is given."""
+    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
+        raise QuickError(QUICK_ERR_INVALID_ARG, "w4a16_gemm: x must be a contiguous [M][K] float16 tensor")
+    M, K = x.shape
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    elif y.dtype != torch.float16 or tuple(y.shape) != (M, N) or not y.is_contiguous():
+        raise QuickError(QUICK_ERR_INVALID_ARG, "w4a16_gemm: y must be a contiguous [M][N] float16 tensor")
+    wb, zb, sb = packed_sizes(K, N, group)
+    for t, nb, name in ((packed, wb, "packed"), (scales, sb, "scales"), (zeros, zb, "zeros")):
+        if not t.is_contiguous() or t.numel() * t.element_size() < nb:
+            raise QuickError(QUICK_ERR_SHAPE, "w4a16_gemm: %s buffer too small or not contiguous" % name)
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    hs = ctypes.c_void_p(st.cuda_stream)
+    if cfg is None and workspace is None:
+        rc = lib().quick_w4a16_gemm(_dptr(x), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y),
+                                    M, N, K, group, hs)
+    else:
+        wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+        rc = lib().quick_w4a16_gemm_ex(_dptr(x), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y),
+                                       M, N, K, group, hs,
+                                       ctypes.byref(cfg) if cfg is not None else None,
+                                       _dptr(workspace), wsb)
+    _check(rc, "quick_w4a16_gemm")
+    return y
+
+
+EXPORTED = (
+    "quick_status_string", "quick_pack_format_version", "quick_packed_sizes", "quick_pack_weights",
+    "quick_unpack_weights", "quick_w4a16_gemm", "quick_w4a16_gemm_ex", "quick_workspace_bytes",
+    "quick_select_config",
+)

@@ -1,0 +1,709 @@
+// W4A16 GEMM kernels for gfx950 (MI355X) and the GEMM entry points of the
+// C ABI.
+//
+// y[M][N] = x[M][K] . W,  W[k][n] = (q[k][n] - z[k/128][n]) * s[k/128][n]
+// (paper, Section 2.1 and Section 2.3), with the weights in the QPK16 packed
+// layout produced offline by quick_pack_weights (Section 3.1, 3.2).
+//
+// Common scheme of both kernels:
+//  * One 16-byte load per lane fetches a lane's share of a 1 KiB packed
+//    unit (16 columns x 128 input channels): 4 words, one per 32-wide k step
+//    of the 16x16x32 f16 matrix instruction.  The words go straight into
+//    VGPRs; dequantized weights never touch LDS (Section 3.1).
+//  * Dequantization in VGPRs with packed f16 arithmetic (Section 2.3):
+//    masking the word and its 8-bit shift with 0x000F000F / 0x00F000F0 and
+//    OR-ing the binary16 pattern of 1024 yields f16 pairs 1024+q (low
+//    nibbles) and 1024+16q (high nibbles); subtracting 1024+z, or fused
+//    multiply-adding with 1/16 and -(64+z), gives q-z exactly, and one f16
+//    multiply by s gives the weight with a single rounding.  The nibble order
+//    inside the word (Section 3.2's dequant-aware reorder) makes the four f16
+//    pairs come out in k order, i.e. already in operand-register order.
+//  * The dequantized weights are the instruction's A operand (rows = output
+//    columns n) and the activations its B operand (columns = rows m of x), so
+//    each lane ends with 4 consecutive n of one output row in its 4
+//    accumulators and stores them as one 8-byte write.
+//  * fp32 accumulation everywhere, including split-K partial sums, and one
+//    final round-to-nearest-even to f16.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <utility>
+
+#include "quick.h"
+#include "quick_internal.h"
+
+namespace {
+
+typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
+typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
+typedef float f4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u2_t __attribute__((ext_vector_type(2)));
+
+constexpr int kUnitScales = 16;   // scales per unit
+constexpr int kUnitZeroWords = 2; // zero-point words per unit
+
+template <class To, class From>
+__device__ __forceinline__ To bits_as(const From& v)
+{
+    static_assert(sizeof(To) == sizeof(From), "size mismatch");
+    return __builtin_bit_cast(To, v);
+}
+
+// Per (column, k-group) constants of the dequantizer, as f16x2 bit patterns:
+// zlo = (1024+z, 1024+z), zhi = (-(64+z), -(64+z)), ss = (s, s).
+struct Deq {
+    uint32_t zlo, zhi, ss;
+};
+
+__device__ __forceinline__ Deq make_deq(uint32_t s_bits, uint32_t z)
+{
+    const uint32_t a = 0x6400u | z;          // binary16 of 1024 + z
+    const uint32_t b = 0xD400u + (z << 4);   // binary16 of -(64 + z), ulp 1/16
+    Deq d;
+    d.zlo = a | (a << 16);
+    d.zhi = b | (b << 16);
+    d.ss = s_bits | (s_bits << 16);
+    return d;
+}
+
+// Eight weights of one packed word -> the 8 f16 operand values, k order.
+__device__ __forceinline__ h8_t dequant8(uint32_t w, const Deq& d)
+{
+#pragma clang fp contract(off)
+    const uint32_t lo = 0x000F000Fu, hi = 0x00F000F0u, one024 = 0x64006400u;
+    const uint32_t w8 = w >> 8;
+    const h2_t h0 = bits_as<h2_t>((w & lo) | one024);   // 1024 + q(e0), 1024 + q(e1)
+    const h2_t h1 = bits_as<h2_t>((w & hi) | one024);   // 1024 + 16 q(e2), ... q(e3)
+    const h2_t h2 = bits_as<h2_t>((w8 & lo) | one024);  // e4, e5
+    const h2_t h3 = bits_as<h2_t>((w8 & hi) | one024);  // e6, e7
+    const h2_t zlo = bits_as<h2_t>(d.zlo);
+    const h2_t zhi = bits_as<h2_t>(d.zhi);
+    const h2_t ss = bits_as<h2_t>(d.ss);
+    const h2_t sixteenth = {(_Float16)0.0625f, (_Float16)0.0625f};
+    const h2_t d0 = (h0 - zlo) * ss;
+    const h2_t d1 = __builtin_elementwise_fma(h1, sixteenth, zhi) * ss;
+    const h2_t d2 = (h2 - zlo) * ss;
+    const h2_t d3 = __builtin_elementwise_fma(h3, sixteenth, zhi) * ss;
+    h8_t r = {d0[0], d0[1], d1[0], d1[1], d2[0], d2[1], d3[0], d3[1]};
+    return r;
+}
+
+__device__ __forceinline__ f4_t mfma16(const h8_t& a, const h8_t& b, const f4_t& c)
+{
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// 4 fp32 -> 4 f16 (round to nearest even), stored as one 8-byte write.
+__device__ __forceinline__ void store_h4(uint16_t* dst, const f4_t& v)
+{
+    const _Float16 a = (_Float16)v[0], b = (_Float16)v[1], c = (_Float16)v[2], e = (_Float16)v[3];
+    u2_t o;
+    o[0] = (uint32_t)bits_as<uint16_t>(a) | ((uint32_t)bits_as<uint16_t>(b) << 16);
+    o[1] = (uint32_t)bits_as<uint16_t>(c) | ((uint32_t)bits_as<uint16_t>(e) << 16);
+    *reinterpret_cast<u2_t*>(dst) = o;
+}
+
+// ---------------------------------------------------------------------------
+// Stream kernel (small M, bandwidth-bound).
+//
+// A workgroup owns NPW n-tiles (16 columns each) and the whole K range; its
+// WAVES waves split the k-groups between them (in-workgroup split-K) and each
+// wave streams its packed units from HBM with one 16-byte load per lane and
+// unit, one k-group ahead of the math.  Activation fragments (MT blocks of 16
+// rows) are read straight from global memory (they are small and shared by
+// every workgroup, so they hit in cache).  At the end the waves' fp32 partial
+// tiles are summed through LDS in wave order (deterministic) and stored.
+// ---------------------------------------------------------------------------
+template <int MT, int NPW>
+struct StreamStage {
+    u4_t w[NPW];
+    uint32_t s[NPW];
+    uint32_t z[NPW];
+    u4_t xf[MT][4];
+};
+
+template <int MT, int NPW, int WAVES>
+__global__ void __launch_bounds__(64 * WAVES)
+stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
+              const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
+              uint16_t* __restrict__ y, int M, int N, int K)
+{
+    const int KG = K >> 7;
+    const int NT = N >> 4;
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int c = lane & 15;
+    const int g = lane >> 4;
+    const int nt0 = blockIdx.x * NPW;
+    const int kb = (KG * wave) / WAVES;
+    const int ke = (KG * (wave + 1)) / WAVES;
+
+    bool nok[NPW];
+#pragma unroll
+    for (int p = 0; p < NPW; ++p) nok[p] = nt0 + p < NT;
+
+    const u4_t* xrow[MT];
+    bool mok[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) {
+        const int m = mt * 16 + c;
+        mok[mt] = m < M;
+        xrow[mt] = reinterpret_cast<const u4_t*>(x + (size_t)(mok[mt] ? m : 0) * K) + g;
+    }
+
+    f4_t acc[NPW][MT];
+#pragma unroll
+    for (int p = 0; p < NPW; ++p)
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) acc[p][mt] = f4_t{0.f, 0.f, 0.f, 0.f};
+
+    auto load = [&](StreamStage<MT, NPW>& st, int kg) {
+#pragma unroll
+        for (int p = 0; p < NPW; ++p) {
+            const size_t unit = (size_t)(nok[p] ? nt0 + p : 0) * KG + kg;
+            st.w[p] = nok[p] ? pw[unit * 64 + lane] : u4_t{0u, 0u, 0u, 0u};
+            st.s[p] = ps[unit * kUnitScales + c];
+            st.z[p] = pz[unit * kUnitZeroWords + (c >> 3)];
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                st.xf[mt][j] = mok[mt] ? xrow[mt][kg * 16 + j * 4] : u4_t{0u, 0u, 0u, 0u};
+    };
+
+    auto compute = [&](const StreamStage<MT, NPW>& st) {
+        Deq d[NPW];
+#pragma unroll
+        for (int p = 0; p < NPW; ++p) d[p] = make_deq(st.s[p], (st.z[p] >> (4 * (c & 7))) & 15u);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int p = 0; p < NPW; ++p) {
+                const h8_t a = dequant8(st.w[p][j], d[p]);
+#pragma unroll
+                for (int mt = 0; mt < MT; ++mt)
+                    acc[p][mt] = mfma16(a, bits_as<h8_t>(st.xf[mt][j]), acc[p][mt]);
+            }
+        }
+    };
+
+    StreamStage<MT, NPW> s0, s1;
+    int kg = kb;
+    if (kg < ke) load(s0, kg);
+    for (; kg + 1 < ke; kg += 2) {
+        load(s1, kg + 1);
+        compute(s0);
+        if (kg + 2 < ke) load(s0, kg + 2);
+        compute(s1);
+    }
+    if (kg < ke) compute(s0);
+
+    if constexpr (WAVES == 1) {
+#pragma unroll
+        for (int p = 0; p < NPW; ++p) {
+            if (!nok[p]) continue;
+            const int n = (nt0 + p) * 16 + 4 * g;
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+                if (mok[mt]) store_h4(y + (size_t)(mt * 16 + c) * N + n, acc[p][mt]);
+        }
+    } else {
+        __shared__ f4_t red[WAVES][NPW * MT][64];
+#pragma unroll
+        for (int p = 0; p < NPW; ++p)
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt) red[wave][p * MT + mt][lane] = acc[p][mt];
+        __syncthreads();
+        for (int item = threadIdx.x; item < NPW * MT * 64; item += 64 * WAVES) {
+            const int l = item & 63;
+            const int pm = item >> 6;
+            const int p = pm / MT;
+            const int mt = pm % MT;
+            const int m = mt * 16 + (l & 15);
+            if (nt0 + p >= NT || m >= M) continue;
+            f4_t sum = red[0][pm][l];
+#pragma unroll
+            for (int w = 1; w < WAVES; ++w) sum += red[w][pm][l];
+            store_h4(y + (size_t)m * N + (nt0 + p) * 16 + 4 * (l >> 4), sum);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Tiled kernel (large M, matrix-core-bound).
+//
+// A workgroup of 4 waves computes a BM x (4*WN) output tile.  The waves split
+// the columns (each wave WN columns, all BM rows), so every packed weight is
+// loaded and dequantized exactly once per workgroup, straight into VGPRs.
+// Only the activation tile (BM rows x 128 input channels, one k-group) is
+// staged in LDS, double-buffered, rows padded by 16 bytes so the 16-byte
+// fragment reads of 16 consecutive rows fall in distinct banks
+// (Section 3.3: LDS holds activations only, which frees it for larger tiles).
+// gridDim.z > 1 splits the k-groups; partial tiles then go to an fp32
+// workspace and a second kernel sums them in split order.
+// ---------------------------------------------------------------------------
+template <int BM, int WN>
+__global__ void __launch_bounds__(256)
+tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
+             const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
+             uint16_t* __restrict__ y, float* __restrict__ ws, int M, int N, int K,
+             int kg_per_split)
+{
+    constexpr int NP = WN / 16;
+    constexpr int MTT = BM / 16;
+    constexpr int XR = BM / 16;   // activation rows each thread stages per k-group
+    constexpr int ROWU = 17;      // u4 per LDS row: 16 data + 1 pad
+    __shared__ u4_t xs[2][BM][ROWU];
+
+    const int KG = K >> 7;
+    const int NT = N >> 4;
+    const int KX = K >> 3;        // u4 per activation row
+    const int lane = threadIdx.x & 63;
+    const int wave = threadIdx.x >> 6;
+    const int c = lane & 15;
+    const int g = lane >> 4;
+    const int ntw = blockIdx.x * (4 * NP) + wave * NP;
+    const int m0 = blockIdx.y * BM;
+    const int kb = blockIdx.z * kg_per_split;
+    const int ke = min(KG, kb + kg_per_split);
+    const int tr = threadIdx.x >> 4;
+    const int tc = threadIdx.x & 15;
+    const u4_t* X4 = reinterpret_cast<const u4_t*>(x);
+
+    bool nok[NP];
+#pragma unroll
+    for (int p = 0; p < NP; ++p) nok[p] = ntw + p < NT;
+
+    u4_t xr[XR];
+    auto load_x = [&](int kg) {
+#pragma unroll
+        for (int i = 0; i < XR; ++i) {
+            const int m = m0 + i * 16 + tr;
+            xr[i] = m < M ? X4[(size_t)m * KX + kg * 16 + tc] : u4_t{0u, 0u, 0u, 0u};
+        }
+    };
+    auto store_x = [&](int buf) {
+#pragma unroll
+        for (int i = 0; i < XR; ++i) xs[buf][i * 16 + tr][tc] = xr[i];
+    };
+
+    u4_t wv[NP];
+    uint32_t sv[NP], zv[NP];
+    auto load_w = [&](u4_t* w, uint32_t* s, uint32_t* z, int kg) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            const size_t unit = (size_t)(nok[p] ? ntw + p : 0) * KG + kg;
+            w[p] = nok[p] ? pw[unit * 64 + lane] : u4_t{0u, 0u, 0u, 0u};
+            s[p] = ps[unit * kUnitScales + c];
+            z[p] = pz[unit * kUnitZeroWords + (c >> 3)];
+        }
+    };
+
+    f4_t acc[NP][MTT];
+#pragma unroll
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+        for (int mt = 0; mt < MTT; ++mt) acc[p][mt] = f4_t{0.f, 0.f, 0.f, 0.f};
+
+    if (kb < ke) {
+        load_x(kb);
+        load_w(wv, sv, zv, kb);
+        store_x(0);
+    }
+    __syncthreads();
+
+    for (int kg = kb; kg < ke; ++kg) {
+        const int buf = (kg - kb) & 1;
+        const bool more = kg + 1 < ke;
+        u4_t wn[NP];
+        uint32_t sn[NP], zn[NP];
+        if (more) {
+            load_x(kg + 1);
+            load_w(wn, sn, zn, kg + 1);
+        }
+        Deq d[NP];
+#pragma unroll
+        for (int p = 0; p < NP; ++p) d[p] = make_deq(sv[p], (zv[p] >> (4 * (c & 7))) & 15u);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            h8_t a[NP];
+#pragma unroll
+            for (int p = 0; p < NP; ++p) a[p] = dequant8(wv[p][j], d[p]);
+#pragma unroll
+            for (int mt = 0; mt < MTT; ++mt) {
+                const h8_t b = bits_as<h8_t>(xs[buf][mt * 16 + c][j * 4 + g]);
+#pragma unroll
+                for (int p = 0; p < NP; ++p) acc[p][mt] = mfma16(a[p], b, acc[p][mt]);
+            }
+        }
+        if (more) {
+            store_x(buf ^ 1);
+#pragma unroll
+            for (int p = 0; p < NP; ++p) {
+                wv[p] = wn[p];
+                sv[p] = sn[p];
+                zv[p] = zn[p];
+            }
+        }
+        __syncthreads();
+    }
+
+    if (gridDim.z == 1) {
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            if (!nok[p]) continue;
+            const int n = (ntw + p) * 16 + 4 * g;
+#pragma unroll
+            for (int mt = 0; mt < MTT; ++mt) {
+                const int m = m0 + mt * 16 + c;
+                if (m < M) store_h4(y + (size_t)m * N + n, acc[p][mt]);
+            }
+        }
+    } else {
+        float* part = ws + (size_t)blockIdx.z * M * N;
+#pragma unroll
+        for (int p = 0; p < NP; ++p) {
+            if (!nok[p]) continue;
+            const int n = (ntw + p) * 16 + 4 * g;
+#pragma unroll
+            for (int mt = 0; mt < MTT; ++mt) {
+                const int m = m0 + mt * 16 + c;
+                if (m < M) *reinterpret_cast<f4_t*>(part + (size_t)m * N + n) = acc[p][mt];
+            }
+        }
+    }
+}
+
+// Sum of S fp32 partial outputs in split order, rounded once to f16.
+__global__ void __launch_bounds__(256)
+splitk_reduce_kernel(const float* __restrict__ ws, uint16_t* __restrict__ y, int64_t MN4, int64_t MN,
+                     int S)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= MN4) return;
+    const f4_t* p = reinterpret_cast<const f4_t*>(ws) + i;
+    f4_t sum = p[0];
+    for (int s = 1; s < S; ++s) sum += p[(size_t)s * (MN / 4)];
+    store_h4(y + i * 4, sum);
+}
+
+// ---------------------------------------------------------------------------
+// Host side: validation, configuration, workspace, launch.
+// ---------------------------------------------------------------------------
+constexpr int kVariantStream = 1;
+constexpr int kVariantTiled = 2;
+
+struct Plan {
+    int variant;
+    int split;  // stream: waves per workgroup; tiled: k splits
+    int bm;     // tiled: rows per workgroup
+    int wn;     // tiled: columns per wave; stream: n-tiles per wave
+    int kgps;   // tiled: k-groups per split
+};
+
+int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
+{
+    const int64_t KG = K / 128;
+    const int64_t NT = N / 16;
+    if (M <= 64) {
+        pl->variant = kVariantStream;
+        pl->wn = NT / 2 >= 512 ? 2 : 1;
+        const int64_t wgs = (NT + pl->wn - 1) / pl->wn;
+        int w = 1;
+        while (w < 8 && wgs * w < 2048 && KG / (2 * w) >= 2) w *= 2;
+        pl->split = w;
+        pl->bm = 0;
+        pl->kgps = 0;
+    } else {
+        pl->variant = kVariantTiled;
+        pl->bm = M <= 96 ? 64 : 128;
+        pl->wn = 64;
+        const int64_t tiles = (int64_t)ceil_div(M, pl->bm) * ceil_div(N, 4 * pl->wn);
+        int s = 1;
+        while (tiles * s < 256 && KG / (2 * s) >= 4) s *= 2;
+        pl->split = s;
+        pl->kgps = 0;
+    }
+    return QUICK_OK;
+}
+
+int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* pl)
+{
+    auto_plan(M, N, K, pl);
+    if (!cfg) return QUICK_OK;
+    const int64_t KG = K / 128;
+    if (cfg->variant < 0 || cfg->variant > 2 || cfg->split_k < 0) return QUICK_ERR_INVALID_ARG;
+    if (cfg->variant == kVariantStream) {
+        if (M > 64) return QUICK_ERR_INVALID_ARG;
+        if (pl->variant != kVariantStream) auto_plan(std::min<int64_t>(M, 64), N, K, pl);
+        pl->variant = kVariantStream;
+        if (cfg->split_k) {
+            if (cfg->split_k != 1 && cfg->split_k != 2 && cfg->split_k != 4 && cfg->split_k != 8)
+                return QUICK_ERR_INVALID_ARG;
+            pl->split = cfg->split_k;
+        }
+        if (cfg->tile_n) {
+            if (cfg->tile_n != 1 && cfg->tile_n != 2) return QUICK_ERR_INVALID_ARG;
+            pl->wn = cfg->tile_n;
+        }
+    } else if (cfg->variant == kVariantTiled) {
+        if (pl->variant != kVariantTiled) {
+            pl->variant = kVariantTiled;
+            pl->bm = 64;
+            pl->wn = 64;
+            pl->split = 1;
+        }
+    }
+    if (pl->variant == kVariantTiled) {
+        if (cfg->tile_m) {
+            if (cfg->tile_m != 64 && cfg->tile_m != 128 && cfg->tile_m != 256) return QUICK_ERR_INVALID_ARG;
+            pl->bm = cfg->tile_m;
+        }
+        if (cfg->tile_n) {
+            if (cfg->tile_n != 32 && cfg->tile_n != 64) return QUICK_ERR_INVALID_ARG;
+            pl->wn = cfg->tile_n;
+        }
+        if (cfg->split_k) {
+            if (cfg->split_k > KG) return QUICK_ERR_INVALID_ARG;
+            pl->split = cfg->split_k;
+        }
+        // 256 x 64-column waves need more than 512 registers per lane.
+        if (pl->bm == 256 && pl->wn == 64) return QUICK_ERR_INVALID_ARG;
+    }
+    return QUICK_OK;
+}
+
+void finish_plan(int64_t K, Plan* pl)
+{
+    if (pl->variant == kVariantTiled) {
+        const int64_t KG = K / 128;
+        if (pl->split > KG) pl->split = (int)KG;
+        if (pl->split < 1) pl->split = 1;
+        pl->kgps = ceil_div(KG, pl->split);
+        pl->split = ceil_div(KG, pl->kgps);  // no empty splits
+    }
+}
+
+size_t plan_workspace(int64_t M, int64_t N, const Plan& pl)
+{
+    if (pl.variant == kVariantTiled && pl.split > 1) return (size_t)pl.split * M * N * sizeof(float);
+    return 0;
+}
+
+// Library-owned split-K workspace, one per (device, stream).
+struct WsKey {
+    int dev;
+    void* stream;
+    bool operator<(const WsKey& o) const { return dev != o.dev ? dev < o.dev : stream < o.stream; }
+};
+struct WsBuf {
+    void* ptr = nullptr;
+    size_t bytes = 0;
+};
+std::mutex g_ws_mu;
+std::map<WsKey, WsBuf> g_ws;
+
+int get_workspace(size_t need, hipStream_t stream, void** out)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return QUICK_ERR_HIP;
+    std::lock_guard<std::mutex> lk(g_ws_mu);
+    WsBuf& b = g_ws[WsKey{dev, (void*)stream}];
+    if (b.bytes < need) {
+        if (b.ptr) {
+            if (hipStreamSynchronize(stream) != hipSuccess) return QUICK_ERR_HIP;
+            (void)hipFree(b.ptr);
+            b.ptr = nullptr;
+            b.bytes = 0;
+        }
+        size_t sz = std::max<size_t>(need, (size_t)1 << 20);
+        if (hipMalloc(&b.ptr, sz) != hipSuccess) {
+            b.ptr = nullptr;
+            return QUICK_ERR_HIP;
+        }
+        b.bytes = sz;
+    }
+    *out = b.ptr;
+    return QUICK_OK;
+}
+
+template <int MT, int NPW, int WAVES>
+void launch_stream_t(const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz,
+                     uint16_t* y, int M, int N, int K, hipStream_t st)
+{
+    const int NT = N / 16;
+    dim3 grid((NT + NPW - 1) / NPW);
+    hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES>), grid, dim3(64 * WAVES), 0, st, x, pw, ps, pz,
+                       y, M, N, K);
+}
+
+template <int MT, int NPW>
+int launch_stream_w(int waves, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
+                    const uint32_t* pz, uint16_t* y, int M, int N, int K, hipStream_t st)
+{
+    switch (waves) {
+    case 1: launch_stream_t<MT, NPW, 1>(x, pw, ps, pz, y, M, N, K, st); break;
+    case 2: launch_stream_t<MT, NPW, 2>(x, pw, ps, pz, y, M, N, K, st); break;
+    case 4: launch_stream_t<MT, NPW, 4>(x, pw, ps, pz, y, M, N, K, st); break;
+    case 8: launch_stream_t<MT, NPW, 8>(x, pw, ps, pz, y, M, N, K, st); break;
+    default: return QUICK_ERR_INVALID_ARG;
+    }
+    return QUICK_OK;
+}
+
+template <int MT>
+int launch_stream_n(int npw, int waves, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
+                    const uint32_t* pz, uint16_t* y, int M, int N, int K, hipStream_t st)
+{
+    if (npw == 1) return launch_stream_w<MT, 1>(waves, x, pw, ps, pz, y, M, N, K, st);
+    if (npw == 2) return launch_stream_w<MT, 2>(waves, x, pw, ps, pz, y, M, N, K, st);
+    return QUICK_ERR_INVALID_ARG;
+}
+
+int launch_stream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
+                  const uint32_t* pz, uint16_t* y, int M, int N, int K, hipStream_t st)
+{
+    const int mt = (M + 15) / 16;
+    switch (mt) {
+    case 1: return launch_stream_n<1>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st);
+    case 2: return launch_stream_n<2>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st);
+    case 3: return launch_stream_n<3>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st);
+    case 4: return launch_stream_n<4>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st);
+    default: return QUICK_ERR_INVALID_ARG;
+    }
+}
+
+template <int BM, int WN>
+void launch_tiled_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
+                    const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st)
+{
+    dim3 grid(ceil_div(N, 4 * WN), ceil_div(M, BM), pl.split);
+    hipLaunchKernelGGL((tiled_kernel<BM, WN>), grid, dim3(256), 0, st, x, pw, ps, pz, y, ws, M, N, K,
+                       pl.kgps);
+}
+
+int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
+                 const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st)
+{
+    if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
+    else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
+    else if (pl.bm == 128 && pl.wn == 32) launch_tiled_t<128, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
+    else if (pl.bm == 128 && pl.wn == 64) launch_tiled_t<128, 64>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
+    else if (pl.bm == 256 && pl.wn == 32) launch_tiled_t<256, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
+    else return QUICK_ERR_INVALID_ARG;
+    if (pl.split > 1) {
+        const int64_t MN = (int64_t)M * N;
+        const int64_t MN4 = MN / 4;
+        hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((MN4 + 255) / 256)), dim3(256), 0, st,
+                           ws, y, MN4, MN, pl.split);
+    }
+    return QUICK_OK;
+}
+
+bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
+
+int validate(const void* x, const void* packed, const void* scales, const void* zeros, void* y,
+             int64_t M, int64_t N, int64_t K, int64_t group)
+{
+    if (group != quick::kGroup) return QUICK_ERR_UNSUPPORTED;
+    if (M < 0 || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return QUICK_ERR_SHAPE;
+    // 32-bit index arithmetic inside the kernels: keep every operand well
+    // inside the range (largest: packed words K*N/8, activations M*K).
+    if (K * N / 8 > ((int64_t)1 << 31) || M * K > ((int64_t)1 << 31) || M * N > ((int64_t)1 << 31) ||
+        M > (1 << 24))
+        return QUICK_ERR_SHAPE;
+    if (M == 0) return QUICK_OK;
+    if (!x || !packed || !scales || !zeros || !y) return QUICK_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(packed, 16) || !aligned(scales, 2) || !aligned(zeros, 4) ||
+        !aligned(y, 8))
+        return QUICK_ERR_ALIGNMENT;
+    return QUICK_OK;
+}
+
+int gemm_impl(const void* x, const void* packed, const void* scales, const void* zeros, void* y,
+              int64_t M, int64_t N, int64_t K, int64_t group, void* stream, const quick_config_t* cfg,
+              void* workspace, size_t workspace_bytes)
+{
+    int st = validate(x, packed, scales, zeros, y, M, N, K, group);
+    if (st) return st;
+    Plan pl;
+    st = make_plan(M, N, K, cfg, &pl);
+    if (st) return st;
+    if (M == 0) return QUICK_OK;
+    finish_plan(K, &pl);
+    hipStream_t hs = (hipStream_t)stream;
+    const size_t need = plan_workspace(M, N, pl);
+    void* ws = nullptr;
+    if (need) {
+        if (workspace) {
+            if (workspace_bytes < need) return QUICK_ERR_WORKSPACE;
+            if (!aligned(workspace, 16)) return QUICK_ERR_ALIGNMENT;
+            ws = workspace;
+        } else {
+            st = get_workspace(need, hs, &ws);
+            if (st) return st;
+        }
+    }
+    const uint16_t* xx = static_cast<const uint16_t*>(x);
+    const u4_t* pw = static_cast<const u4_t*>(packed);
+    const uint16_t* ps = static_cast<const uint16_t*>(scales);
+    const uint32_t* pz = static_cast<const uint32_t*>(zeros);
+    uint16_t* yy = static_cast<uint16_t*>(y);
+    (void)hipGetLastError();  // clear a stale error so the check below is ours
+    if (pl.variant == kVariantStream)
+        st = launch_stream(pl, xx, pw, ps, pz, yy, (int)M, (int)N, (int)K, hs);
+    else
+        st = launch_tiled(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs);
+    if (st) return st;
+    if (hipGetLastError() != hipSuccess) return QUICK_ERR_HIP;
+    return QUICK_OK;
+}
+
+}  // namespace
+
+extern "C" int quick_w4a16_gemm(const void* x, const void* packed, const void* scales,
+                                const void* zeros, void* y, int64_t M, int64_t N, int64_t K,
+                                int64_t group, void* stream)
+{
+    return gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, nullptr, nullptr, 0);
+}
+
+extern "C" int quick_w4a16_gemm_ex(const void* x, const void* packed, const void* scales,
+                                   const void* zeros, void* y, int64_t M, int64_t N, int64_t K,
+                                   int64_t group, void* stream, const quick_config_t* cfg,
+                                   void* workspace, size_t workspace_bytes)
+{
+    return gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, cfg, workspace,
+                     workspace_bytes);
+}
+
+extern "C" size_t quick_workspace_bytes(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg)
+{
+    if (M <= 0 || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return 0;
+    Plan pl;
+    if (make_plan(M, N, K, cfg, &pl)) return 0;
+    finish_plan(K, &pl);
+    return plan_workspace(M, N, pl);
+}
+
+extern "C" int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config_t* cfg)
+{
+    if (!cfg) return QUICK_ERR_INVALID_ARG;
+    if (M < 0 || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return QUICK_ERR_SHAPE;
+    Plan pl;
+    auto_plan(M, N, K, &pl);
+    finish_plan(K, &pl);
+    cfg->variant = pl.variant;
+    cfg->split_k = pl.split;
+    cfg->tile_m = pl.variant == kVariantTiled ? pl.bm : 0;
+    cfg->tile_n = pl.wn;
+    return QUICK_OK;
+}

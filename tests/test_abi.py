@@ -1,0 +1,122 @@
+"""The C ABI without a GPU: the library loads, exports every function that
+include/quick.h declares, the header compiles as plain C, and every
+validation path returns its status before touching the device."""
+import ctypes
+import os
+import re
+import subprocess
+import tempfile
+
+import numpy as np
+import pytest
+
+import paper_2402_10076_amd as Q
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "quick.h")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(quick_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert "quick_w4a16_gemm" in names and "quick_pack_weights" in names
+    L = Q.lib()
+    for n in names:
+        assert hasattr(L, n), "libquick.so does not export %s" % n
+    assert set(names) == set(Q.EXPORTED)
+
+
+def test_header_is_plain_c_and_links():
+    prog = r'''
+#include "quick.h"
+#include <stdio.h>
+#include <string.h>
+int main(void) {
+    size_t a, b, c;
+    if (quick_pack_format_version() != 1) return 1;
+    if (quick_packed_sizes(256, 32, 128, &a, &b, &c) != QUICK_OK) return 2;
+    if (a != 4096 || b != 32 || c != 128) return 3;
+    if (quick_packed_sizes(256, 32, 64, &a, &b, &c) != QUICK_ERR_UNSUPPORTED) return 4;
+    quick_config_t cfg;
+    memset(&cfg, 0, sizeof cfg);
+    if (quick_select_config(1, 4096, 4096, &cfg) != QUICK_OK || cfg.variant != 1) return 5;
+    if (quick_w4a16_gemm(0, 0, 0, 0, 0, 0, 4096, 4096, 128, 0) != QUICK_OK) return 6;
+    printf("%s\n", quick_status_string(QUICK_ERR_SHAPE));
+    return 0;
+}
+'''
+    with tempfile.TemporaryDirectory() as d:
+        c = os.path.join(d, "t.c")
+        exe = os.path.join(d, "t")
+        open(c, "w").write(prog)
+        libdir = os.path.dirname(Q.LIB_PATH)
+        subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-I", os.path.join(ROOT, "include"), c,
+                        "-o", exe, os.path.join(libdir, "libquick.so"),
+                        "-Wl,-rpath," + libdir], check=True)
+        r = subprocess.run([exe], capture_output=True, text=True)
+        assert r.returncode == 0, r.stdout + r.stderr
+        assert "QUICK_ERR_SHAPE" in r.stdout
+
+
+def _gemm(x, pw, ps, pz, y, M, N, K, group=128):
+    return Q.lib().quick_w4a16_gemm(x, pw, ps, pz, y, M, N, K, group, None)
+
+
+def test_gemm_validation_without_device():
+    A = 0x10000  # fake, 256-byte aligned addresses: never dereferenced
+    ok = dict(x=A, pw=A, ps=A, pz=A, y=A)
+    assert _gemm(**ok, M=0, N=4096, K=4096) == Q.QUICK_OK
+    assert _gemm(0, 0, 0, 0, 0, 0, 4096, 4096) == Q.QUICK_OK
+    assert _gemm(**ok, M=-1, N=4096, K=4096) == Q.QUICK_ERR_SHAPE
+    assert _gemm(**ok, M=4, N=4096, K=4000) == Q.QUICK_ERR_SHAPE
+    assert _gemm(**ok, M=4, N=4088, K=4096) == Q.QUICK_ERR_SHAPE
+    assert _gemm(**ok, M=4, N=0, K=4096) == Q.QUICK_ERR_SHAPE
+    assert _gemm(**ok, M=4, N=4096, K=4096, group=64) == Q.QUICK_ERR_UNSUPPORTED
+    assert _gemm(0, A, A, A, A, 4, 4096, 4096) == Q.QUICK_ERR_INVALID_ARG
+    assert _gemm(A, A, A, A, 0, 4, 4096, 4096) == Q.QUICK_ERR_INVALID_ARG
+    assert _gemm(A + 8, A, A, A, A, 4, 4096, 4096) == Q.QUICK_ERR_ALIGNMENT
+    assert _gemm(A, A + 4, A, A, A, 4, 4096, 4096) == Q.QUICK_ERR_ALIGNMENT
+    assert _gemm(A, A, A + 1, A, A, 4, 4096, 4096) == Q.QUICK_ERR_ALIGNMENT
+    assert _gemm(A, A, A, A + 2, A, 4, 4096, 4096) == Q.QUICK_ERR_ALIGNMENT
+    assert _gemm(A, A, A, A, A + 4, 4, 4096, 4096) == Q.QUICK_ERR_ALIGNMENT
+    # 32-bit index limits
+    assert _gemm(**ok, M=4, N=1 << 20, K=1 << 17) == Q.QUICK_ERR_SHAPE
+
+
+def test_gemm_ex_validation_without_device():
+    A = 0x10000
+    L = Q.lib()
+    def ex(cfg, M=4, N=4096, K=4096, ws=None, wsb=0):
+        return L.quick_w4a16_gemm_ex(A, A, A, A, A, M, N, K, 128, None, ctypes.byref(cfg), ws, wsb)
+    assert ex(Q.make_config(variant=3)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=1), M=65) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=1, split_k=3)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=1, tile_n=3)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=2, tile_m=96)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=2, tile_n=48)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=2, split_k=33)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=2, tile_m=256, tile_n=64)) == Q.QUICK_ERR_INVALID_ARG
+    cfg = Q.make_config(variant=2, tile_m=128, tile_n=64, split_k=4)
+    need = Q.workspace_bytes(256, 4096, 4096, cfg)
+    assert need == 4 * 256 * 4096 * 4
+    assert ex(cfg, M=256, ws=A, wsb=need - 1) == Q.QUICK_ERR_WORKSPACE
+    assert ex(cfg, M=256, ws=A + 4, wsb=need) == Q.QUICK_ERR_ALIGNMENT
+
+
+def test_select_config_regimes():
+    small = Q.select_config(1, 8192, 8192)
+    large = Q.select_config(1024, 8192, 8192)
+    assert small["variant"] == Q.VARIANT_STREAM
+    assert large["variant"] == Q.VARIANT_TILED
+    assert Q.workspace_bytes(1, 8192, 8192) == 0
+
+
+def test_status_strings():
+    for st in range(8):
+        assert Q.status_string(st).startswith("QUICK_")
+    assert "unknown" in Q.status_string(99)

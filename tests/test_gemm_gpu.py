@@ -1,0 +1,168 @@
+"""Parity of the HIP GEMM (through the C ABI) with the CPU oracle.
+
+* every kernel variant, tile and split on ragged shapes that span several
+  tiles and a partial tail, element by element against the oracle;
+* exact cases: one-hot activations give RNE_f16((q - z) * s) bit for bit;
+  integer data give the integer GEMM bit for bit under any split order;
+* metamorphic properties: doubling the scales doubles y exactly, permuting
+  rows of x permutes rows of y exactly, permuting whole 16-column tiles of
+  (q, z, s) permutes columns of y exactly; run-to-run determinism; guard
+  rows around y stay untouched; caller workspace and non-default stream.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2402_10076_amd as Q
+from gpu_util import TOL, Packed, f16_values, from_dev_y, rand_case, rel_err, run, say, to_dev_x
+
+pytestmark = pytest.mark.gpu
+
+STREAM_CFGS = [dict(variant=1, split_k=w, tile_n=p) for w in (1, 2, 4, 8) for p in (1, 2)]
+TILED_CFGS = [dict(variant=2, tile_m=bm, tile_n=wn, split_k=s)
+              for bm, wn in ((64, 32), (64, 64), (128, 32), (128, 64), (256, 32)) for s in (1, 3)]
+
+
+def _check(M, K, N, cfg, seed):
+    say("case M=%d K=%d N=%d cfg=%s" % (M, K, N, cfg))
+    x, q, z, s = rand_case(seed, M, K, N)
+    y = run(x, q, z, s, Q.make_config(**cfg) if cfg else None)
+    ref = oracle.gemm(x, q, z, s)
+    err = rel_err(y, ref)
+    assert err <= TOL, "rel err %.3g for M=%d K=%d N=%d cfg=%s" % (err, M, K, N, cfg)
+    return err
+
+
+@pytest.mark.parametrize("cfg", STREAM_CFGS, ids=lambda c: "w%d_p%d" % (c["split_k"], c["tile_n"]))
+@pytest.mark.parametrize("M", [1, 3, 16, 17, 33, 64])
+def test_stream_variants(M, cfg):
+    for K, N in ((384, 48), (1152, 80)):
+        _check(M, K, N, cfg, seed=M * 1000 + K + N)
+
+
+@pytest.mark.parametrize("cfg", TILED_CFGS, ids=lambda c: "bm%d_wn%d_s%d" % (c["tile_m"], c["tile_n"], c["split_k"]))
+@pytest.mark.parametrize("M", [1, 65, 129, 300])
+def test_tiled_variants(M, cfg):
+    for K, N in ((384, 80), (640, 528)):
+        _check(M, K, N, cfg, seed=M * 1000 + K + N + 7)
+
+
+@pytest.mark.parametrize("M", [1, 2, 5, 16, 31, 64, 65, 96, 127, 200, 513])
+def test_auto_config_small_shapes(M):
+    _check(M, 1024, 272, None, seed=M)
+
+
+def test_c1_toy_full_output():
+    """16 x 512 x 512, group 128, full output against the oracle."""
+    import workloads as W
+    x, q, z, s = W.shape_inputs(W.C1, 0, 16)
+    y = run(x, q, z, s)
+    err = rel_err(y, oracle.gemm(x, q, z, s))
+    say("C1 rel err %.3g" % err)
+    assert err <= TOL
+
+
+@pytest.mark.parametrize("cfg", [None, dict(variant=1, split_k=4, tile_n=2), dict(variant=2, tile_m=64, tile_n=32, split_k=2),
+                                 dict(variant=2, tile_m=128, tile_n=64, split_k=1)])
+def test_one_hot_rows_give_exact_dequant(cfg):
+    """x row m = e_{k_m}: y[m][n] is a single product, so it must equal the
+    binary16 rounding of (q - z) * s exactly."""
+    K, N = 512, 96
+    M = 16 if cfg is None or cfg["variant"] == 1 else 100
+    g = np.random.Generator(np.random.PCG64(5))
+    _, q, z, s = rand_case(6, 1, K, N)
+    ks = g.choice(K, size=M, replace=False)
+    x = np.zeros((M, K), np.uint16)
+    x[np.arange(M), ks] = 0x3C00
+    y = run(x, q, z, s, Q.make_config(**cfg) if cfg else None)
+    W = oracle.dequant(q, z, s)
+    want = oracle.f64_to_f16(W[ks])
+    assert np.array_equal(y, want), "dequantized value mismatch at %d entries" % int((y != want).sum())
+
+
+@pytest.mark.parametrize("cfg", [None] + STREAM_CFGS[::3] + TILED_CFGS[::3])
+def test_integer_data_exact_under_any_split(cfg):
+    """s = 1, z = 8, q in {7,8,9}, x in {-1,0,1}: every partial sum is a small
+    integer, so any summation order is exact and y equals int64 x . (q - z)."""
+    M = 48 if cfg is None or cfg["variant"] == 1 else 150
+    K, N = 1024, 80
+    g = np.random.Generator(np.random.PCG64(9))
+    xi = g.integers(-1, 2, (M, K))
+    qi = g.integers(7, 10, (K, N))
+    ref = xi @ (qi - 8)
+    assert np.abs(ref).max() <= 2048
+    x = xi.astype(np.float16).view(np.uint16)
+    z = np.full((K // 128, N), 8, np.uint8)
+    s = np.full((K // 128, N), 0x3C00, np.uint16)
+    y = run(x, qi.astype(np.uint8), z, s, Q.make_config(**cfg) if cfg else None)
+    assert np.array_equal(f16_values(y), ref.astype(np.float64))
+
+
+@pytest.mark.parametrize("M", [7, 64, 200])
+def test_metamorphic_scale_rows_tiles(M):
+    K, N = 768, 96
+    x, q, z, s = rand_case(11 + M, M, K, N)
+    p = Packed(q, z, s)
+    xd = to_dev_x(x)
+    y = from_dev_y(p.gemm(xd))
+    # doubling the scales doubles y exactly (outside the binary16 subnormal band)
+    s2 = (f16_values(s) * 2).astype(np.float16).view(np.uint16)
+    y2 = run(x, q, z, s2)
+    yv, y2v = f16_values(y), f16_values(y2)
+    keep = np.abs(yv) >= 2.0 ** -14
+    assert np.array_equal(y2v[keep], 2 * yv[keep])
+    # permuting rows of x permutes rows of y
+    perm = np.random.Generator(np.random.PCG64(M)).permutation(M)
+    yp = from_dev_y(p.gemm(to_dev_x(x[perm])))
+    assert np.array_equal(yp, y[perm])
+    # permuting whole 16-column tiles of (q, z, s) permutes columns of y
+    tperm = np.random.Generator(np.random.PCG64(M + 1)).permutation(N // 16)
+    cols = (tperm[:, None] * 16 + np.arange(16)[None, :]).reshape(-1)
+    yt = run(x, q[:, cols], z[:, cols], s[:, cols])
+    assert np.array_equal(yt, y[:, cols])
+    # determinism
+    for _ in range(3):
+        assert np.array_equal(from_dev_y(p.gemm(xd)), y)
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("M", [5, 130])
+def test_guard_rows_untouched(M):
+    K, N = 512, 64
+    x, q, z, s = rand_case(21, M, K, N)
+    p = Packed(q, z, s)
+    big = torch.full((M + 2, N), float("nan"), dtype=torch.float16, device="cuda")
+    p.gemm(to_dev_x(x), y=big[1:M + 1])
+    torch.cuda.synchronize()
+    out = big.cpu()
+    assert torch.isnan(out[0]).all() and torch.isnan(out[M + 1]).all()
+    assert rel_err(from_dev_y(out[1:M + 1].contiguous()), oracle.gemm(x, q, z, s)) <= TOL
+
+
+def test_caller_workspace_and_side_stream():
+    M, K, N = 192, 1024, 256
+    x, q, z, s = rand_case(31, M, K, N)
+    p = Packed(q, z, s)
+    xd = to_dev_x(x)
+    cfg = Q.make_config(variant=2, tile_m=64, tile_n=32, split_k=4)
+    y_int = from_dev_y(p.gemm(xd, cfg=cfg))
+    need = Q.workspace_bytes(M, N, K, cfg)
+    assert need > 0
+    ws = torch.empty(need // 4, dtype=torch.float32, device="cuda")
+    side = torch.cuda.Stream()
+    with torch.cuda.stream(side):
+        y_ws = p.gemm(xd, cfg=cfg, workspace=ws, stream=side)
+    side.synchronize()
+    assert np.array_equal(from_dev_y(y_ws), y_int)
+    small = torch.empty(need // 8, dtype=torch.float32, device="cuda")
+    with pytest.raises(Q.QuickError):
+        p.gemm(xd, cfg=cfg, workspace=small)
+
+
+def test_m_zero_is_noop():
+    K, N = 256, 32
+    _, q, z, s = rand_case(1, 1, K, N)
+    p = Packed(q, z, s)
+    y = p.gemm(torch.empty((0, K), dtype=torch.float16, device="cuda"))
+    assert tuple(y.shape) == (0, N)

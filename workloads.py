@@ -149,15 +149,28 @@ def mixtral_w2_input(expert: int, M: int) -> np.ndarray:
 
 
 def sample_columns(N: int, n_sample: int = 1024, seed: int = 0) -> np.ndarray:
-    """Column sample for large shapes: first 256, last 256 and 512 random
-    columns (sorted, distinct).  All columns when N <= n_sample."""
+    """Column sample for large shapes: the first and last n_sample/4 columns
+    and n_sample/2 random ones in between (sorted, distinct); all columns when
+    N <= n_sample."""
     if N <= n_sample:
         return np.arange(N, dtype=np.int64)
+    e = n_sample // 4
     g = np.random.Generator(np.random.PCG64([seed, N, 7]))
-    head = np.arange(256)
-    tail = np.arange(N - 256, N)
-    mid = g.choice(np.arange(256, N - 256), size=n_sample - 512, replace=False)
+    head = np.arange(e)
+    tail = np.arange(N - e, N)
+    mid = g.choice(np.arange(e, N - e), size=n_sample - 2 * e, replace=False)
     return np.unique(np.concatenate([head, tail, mid])).astype(np.int64)
+
+
+def sample_rows(M: int, n_sample: int = 64, seed: int = 0) -> np.ndarray:
+    """Row sample: all rows when M <= n_sample, else the first and last
+    n_sample/4 rows and n_sample/2 random ones in between."""
+    if M <= n_sample:
+        return np.arange(M, dtype=np.int64)
+    e = n_sample // 4
+    g = np.random.Generator(np.random.PCG64([seed, M, 11]))
+    mid = g.choice(np.arange(e, M - e), size=n_sample - 2 * e, replace=False)
+    return np.unique(np.concatenate([np.arange(e), np.arange(M - e, M), mid])).astype(np.int64)
 
 
 def alg_bytes(M: int, N: int, K: int, group: int = GROUP) -> int:
