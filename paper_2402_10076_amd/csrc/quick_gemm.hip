@@ -44,8 +44,6 @@ typedef float f4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u2_t __attribute__((ext_vector_type(2)));
 
-constexpr int kUnitScales = 16;   // scales per unit
-constexpr int kUnitZeroWords = 2; // zero-point words per unit
 
 template <class To, class From>
 __device__ __forceinline__ To bits_as(const From& v)
@@ -71,16 +69,26 @@ __device__ __forceinline__ Deq make_deq(uint32_t s_bits, uint32_t z)
     return d;
 }
 
+// (a & mask) | bits in one VALU instruction.  gfx9 VOP3 encodings take no
+// literal constants, so the compiler otherwise splits this into an AND and an
+// OR with literals; the mask is passed in an SGPR, the OR pattern in a VGPR.
+__device__ __forceinline__ uint32_t and_or(uint32_t a, uint32_t mask, uint32_t bits)
+{
+    uint32_t r;
+    asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "s"(mask), "v"(bits));
+    return r;
+}
+
 // Eight weights of one packed word -> the 8 f16 operand values, k order.
 __device__ __forceinline__ h8_t dequant8(uint32_t w, const Deq& d)
 {
 #pragma clang fp contract(off)
     const uint32_t lo = 0x000F000Fu, hi = 0x00F000F0u, one024 = 0x64006400u;
     const uint32_t w8 = w >> 8;
-    const h2_t h0 = bits_as<h2_t>((w & lo) | one024);   // 1024 + q(e0), 1024 + q(e1)
-    const h2_t h1 = bits_as<h2_t>((w & hi) | one024);   // 1024 + 16 q(e2), ... q(e3)
-    const h2_t h2 = bits_as<h2_t>((w8 & lo) | one024);  // e4, e5
-    const h2_t h3 = bits_as<h2_t>((w8 & hi) | one024);  // e6, e7
+    const h2_t h0 = bits_as<h2_t>(and_or(w, lo, one024));   // 1024 + q(e0), 1024 + q(e1)
+    const h2_t h1 = bits_as<h2_t>(and_or(w, hi, one024));   // 1024 + 16 q(e2), ... q(e3)
+    const h2_t h2 = bits_as<h2_t>(and_or(w8, lo, one024));  // e4, e5
+    const h2_t h3 = bits_as<h2_t>(and_or(w8, hi, one024));  // e6, e7
     const h2_t zlo = bits_as<h2_t>(d.zlo);
     const h2_t zhi = bits_as<h2_t>(d.zhi);
     const h2_t ss = bits_as<h2_t>(d.ss);
@@ -108,53 +116,99 @@ __device__ __forceinline__ void store_h4(uint16_t* dst, const f4_t& v)
     *reinterpret_cast<u2_t*>(dst) = o;
 }
 
+// Raw buffer loads: a wave-uniform 128-bit descriptor (base, byte size) in
+// SGPRs, a per-lane byte offset in a VGPR and a wave-uniform byte offset in an
+// SGPR, so per-iteration address arithmetic is scalar.  Offsets at or beyond
+// the size read as zero instead of faulting.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr int kRawBufferWord3 = 0x00020000;  // gfx9 raw (untyped, unswizzled) buffer
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)bytes, kRawBufferWord3);
+}
+__device__ __forceinline__ u4_t ld128(rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    return bits_as<u4_t>(__builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ uint32_t ld32(rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    return (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+}
+// 16 bytes per lane from a buffer straight into LDS: lane L of the wave
+// writes bytes [16L, 16L+16) after the wave-uniform LDS address `dst`.
+__device__ __forceinline__ void dma16(rsrc_t r, void* dst, uint32_t voff, uint32_t soff)
+{
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)dst, 16, voff, soff, 0, 0);
+}
+// Wait until every outstanding memory operation of this wave has completed.
+__device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0); }
+// Scheduling fence: no instruction moves across it.
+__device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
+__device__ __forceinline__ uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ __forceinline__ uint32_t ld16(rsrc_t r, uint32_t voff, uint32_t soff)
+{
+    return (uint32_t)(uint16_t)__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+}
+
 // ---------------------------------------------------------------------------
 // Stream kernel (small M, bandwidth-bound).
 //
 // A workgroup owns NPW n-tiles (16 columns each) and the whole K range; its
-// WAVES waves split the k-groups between them (in-workgroup split-K) and each
+// WAVES waves split the k-groups between them (in-workgroup split-K).  Each
 // wave streams its packed units from HBM with one 16-byte load per lane and
-// unit, one k-group ahead of the math.  Activation fragments (MT blocks of 16
-// rows) are read straight from global memory (they are small and shared by
-// every workgroup, so they hit in cache).  At the end the waves' fp32 partial
-// tiles are summed through LDS in wave order (deterministic) and stored.
+// unit through a ring of D register stages, so D k-groups of weights are in
+// flight while one is dequantized and multiplied.  Activation fragments (MT
+// blocks of 16 rows) are read from global memory one k-group ahead (they are
+// small and shared by every workgroup, so they hit in cache).  At the end the
+// waves' fp32 partial tiles are summed through LDS in wave order
+// (deterministic) and stored.
 // ---------------------------------------------------------------------------
-template <int MT, int NPW>
-struct StreamStage {
+template <int NPW>
+struct WStage {
     u4_t w[NPW];
     uint32_t s[NPW];
     uint32_t z[NPW];
-    u4_t xf[MT][4];
 };
 
-template <int MT, int NPW, int WAVES>
+template <int MT, int NPW, int WAVES, int D>
 __global__ void __launch_bounds__(64 * WAVES)
 stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
               const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
               uint16_t* __restrict__ y, int M, int N, int K)
 {
+    static_assert(D % 2 == 0, "ring depth must be even (activation double buffer parity)");
     const int KG = K >> 7;
     const int NT = N >> 4;
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    // wave index as a scalar: everything derived from it (k range, buffer
+    // offsets) stays in SGPRs
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int c = lane & 15;
     const int g = lane >> 4;
     const int nt0 = blockIdx.x * NPW;
     const int kb = (KG * wave) / WAVES;
     const int ke = (KG * (wave + 1)) / WAVES;
 
-    bool nok[NPW];
-#pragma unroll
-    for (int p = 0; p < NPW; ++p) nok[p] = nt0 + p < NT;
+    const rsrc_t rw = make_rsrc(pw, (uint32_t)((size_t)K * N / 2));
+    const rsrc_t rs = make_rsrc(ps, (uint32_t)((size_t)K * N / 64));
+    const rsrc_t rz = make_rsrc(pz, (uint32_t)((size_t)K * N / 256));
+    const rsrc_t rx = make_rsrc(x, (uint32_t)((size_t)M * K * 2));
 
-    const u4_t* xrow[MT];
-    bool mok[MT];
+    // Column tiles past the end of N and activation rows past M are clamped
+    // to valid ones instead of masked: an output row of the instruction
+    // depends only on its own weight row (n) and an output column only on
+    // its own activation column (m), and those outputs are never stored.
+    uint32_t ubase[NPW];  // first unit of each n-tile, wave-uniform
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) {
-        const int m = mt * 16 + c;
-        mok[mt] = m < M;
-        xrow[mt] = reinterpret_cast<const u4_t*>(x + (size_t)(mok[mt] ? m : 0) * K) + g;
-    }
+    for (int p = 0; p < NPW; ++p) ubase[p] = (uint32_t)min(nt0 + p, NT - 1) * KG;
+    const uint32_t vw = lane * 16;
+    const uint32_t vs = c * 2;
+    const uint32_t vz = (c >> 3) * 4;
+    uint32_t vx[MT];
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt) vx[mt] = (uint32_t)(min(mt * 16 + c, M - 1) * K + g * 8) * 2;
 
     f4_t acc[NPW][MT];
 #pragma unroll
@@ -162,22 +216,25 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt) acc[p][mt] = f4_t{0.f, 0.f, 0.f, 0.f};
 
-    auto load = [&](StreamStage<MT, NPW>& st, int kg) {
+    WStage<NPW> ring[D];
+    u4_t xf[2][MT][4];
+
+    auto load_w = [&](WStage<NPW>& st, int kg) {
 #pragma unroll
         for (int p = 0; p < NPW; ++p) {
-            const size_t unit = (size_t)(nok[p] ? nt0 + p : 0) * KG + kg;
-            st.w[p] = nok[p] ? pw[unit * 64 + lane] : u4_t{0u, 0u, 0u, 0u};
-            st.s[p] = ps[unit * kUnitScales + c];
-            st.z[p] = pz[unit * kUnitZeroWords + (c >> 3)];
+            const uint32_t u = ubase[p] + kg;
+            st.w[p] = ld128(rw, vw, u * 1024u);
+            st.s[p] = ld16(rs, vs, u * 32u);
+            st.z[p] = ld32(rz, vz, u * 8u);
         }
+    };
+    auto load_x = [&](u4_t (&xb)[MT][4], int kg) {
 #pragma unroll
         for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                st.xf[mt][j] = mok[mt] ? xrow[mt][kg * 16 + j * 4] : u4_t{0u, 0u, 0u, 0u};
+            for (int j = 0; j < 4; ++j) xb[mt][j] = ld128(rx, vx[mt] + j * 64, kg * 256u);
     };
-
-    auto compute = [&](const StreamStage<MT, NPW>& st) {
+    auto compute = [&](const WStage<NPW>& st, const u4_t (&xb)[MT][4]) {
         Deq d[NPW];
 #pragma unroll
         for (int p = 0; p < NPW; ++p) d[p] = make_deq(st.s[p], (st.z[p] >> (4 * (c & 7))) & 15u);
@@ -188,30 +245,36 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
                 const h8_t a = dequant8(st.w[p][j], d[p]);
 #pragma unroll
                 for (int mt = 0; mt < MT; ++mt)
-                    acc[p][mt] = mfma16(a, bits_as<h8_t>(st.xf[mt][j]), acc[p][mt]);
+                    acc[p][mt] = mfma16(a, bits_as<h8_t>(xb[mt][j]), acc[p][mt]);
             }
         }
     };
 
-    StreamStage<MT, NPW> s0, s1;
-    int kg = kb;
-    if (kg < ke) load(s0, kg);
-    for (; kg + 1 < ke; kg += 2) {
-        load(s1, kg + 1);
-        compute(s0);
-        if (kg + 2 < ke) load(s0, kg + 2);
-        compute(s1);
+#pragma unroll
+    for (int i = 0; i < D; ++i)
+        if (kb + i < ke) load_w(ring[i], kb + i);
+    if (kb < ke) load_x(xf[0], kb);
+
+    for (int kg = kb; kg < ke; kg += D) {
+#pragma unroll
+        for (int i = 0; i < D; ++i) {
+            const int k = kg + i;
+            if (k < ke) {
+                if (k + 1 < ke) load_x(xf[(i + 1) & 1], k + 1);
+                compute(ring[i], xf[i & 1]);
+                if (k + D < ke) load_w(ring[i], k + D);
+            }
+        }
     }
-    if (kg < ke) compute(s0);
 
     if constexpr (WAVES == 1) {
 #pragma unroll
         for (int p = 0; p < NPW; ++p) {
-            if (!nok[p]) continue;
+            if (nt0 + p >= NT) continue;
             const int n = (nt0 + p) * 16 + 4 * g;
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt)
-                if (mok[mt]) store_h4(y + (size_t)(mt * 16 + c) * N + n, acc[p][mt]);
+                if (mt * 16 + c < M) store_h4(y + (size_t)(mt * 16 + c) * N + n, acc[p][mt]);
         }
     } else {
         __shared__ f4_t red[WAVES][NPW * MT][64];
@@ -238,70 +301,107 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 // ---------------------------------------------------------------------------
 // Tiled kernel (large M, matrix-core-bound).
 //
-// A workgroup of 4 waves computes a BM x (4*WN) output tile.  The waves split
-// the columns (each wave WN columns, all BM rows), so every packed weight is
-// loaded and dequantized exactly once per workgroup, straight into VGPRs.
-// Only the activation tile (BM rows x 128 input channels, one k-group) is
-// staged in LDS, double-buffered, rows padded by 16 bytes so the 16-byte
-// fragment reads of 16 consecutive rows fall in distinct banks
-// (Section 3.3: LDS holds activations only, which frees it for larger tiles).
-// gridDim.z > 1 splits the k-groups; partial tiles then go to an fp32
-// workspace and a second kernel sums them in split order.
+// A workgroup of 4 waves computes a BM x (4*WN) output tile; the waves split
+// the columns (each wave WN columns and all BM rows), so every packed weight
+// is loaded and dequantized exactly once per workgroup, straight into VGPRs
+// (Section 3.1), and the only LDS traffic is the activation tile
+// (Section 3.3: LDS holds activations only, which leaves room for big tiles).
+//
+// Activation tile: BM rows x 128 input channels (one k-group) per stage, two
+// stages.  It is copied global -> LDS by the 16-byte LDS-DMA form of the
+// buffer load (no staging registers): one instruction moves 4 rows, lane L
+// landing at byte 16*L of the instruction's 1 KiB.  Inside a 256-byte row the
+// 16-byte chunk holding channels 8*q .. 8*q+7 sits at position q ^ (row % 16),
+// so the fragment reads of 16 consecutive rows at one chunk index hit 16
+// distinct bank groups.
+//
+// Weights: one 16-byte load per lane and n-tile per k-group, into a
+// two-stage register ring filled one k-group ahead.  Within a k-group the
+// dequantization of step j+1 is issued between the matrix instructions of
+// step j by the scheduler (two waves per SIMD where registers allow).
+//
+// Tiles are numbered M-fastest and assigned so that consecutive numbers run
+// on the same XCD (hardware hands workgroup ids to the 8 XCDs round-robin):
+// the M-tiles sharing an N-tile's weights then share one L2.
+// gridDim.x > tiles*splits pads to a multiple of 8; those workgroups exit.
+// With splits > 1 each split writes fp32 partial sums to the workspace and a
+// second kernel adds them in split order.
 // ---------------------------------------------------------------------------
-template <int BM, int WN>
-__global__ void __launch_bounds__(256)
+template <int BM, int WN, int MINW>
+__global__ void __launch_bounds__(256, MINW)
 tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
              const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
              uint16_t* __restrict__ y, float* __restrict__ ws, int M, int N, int K,
-             int kg_per_split)
+             int kg_per_split, int n_mtiles, int n_ntiles, int n_splits)
 {
-    constexpr int NP = WN / 16;
-    constexpr int MTT = BM / 16;
-    constexpr int XR = BM / 16;   // activation rows each thread stages per k-group
-    constexpr int ROWU = 17;      // u4 per LDS row: 16 data + 1 pad
-    __shared__ u4_t xs[2][BM][ROWU];
+    constexpr int NP = WN / 16;         // n-tiles per wave
+    constexpr int MTT = BM / 16;        // 16-row blocks per workgroup
+    constexpr int ROWB = 256;           // bytes per activation row of a stage
+    constexpr int STAGE = BM * ROWB;    // bytes per stage
+    constexpr int DMA_PER_WAVE = BM / 16;  // 1 KiB LDS-DMA instructions per wave and stage
+    __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * STAGE];
+
+    // ---- tile assignment (XCD-aware, M-fastest)
+    const int nblk = n_mtiles * n_ntiles * n_splits;
+    const int per_xcd = gridDim.x >> 3;
+    const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+    if (t >= nblk) return;
+    const int mtile = t % n_mtiles;
+    const int ntile = (t / n_mtiles) % n_ntiles;
+    const int split = t / (n_mtiles * n_ntiles);
 
     const int KG = K >> 7;
     const int NT = N >> 4;
-    const int KX = K >> 3;        // u4 per activation row
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int c = lane & 15;
     const int g = lane >> 4;
-    const int ntw = blockIdx.x * (4 * NP) + wave * NP;
-    const int m0 = blockIdx.y * BM;
-    const int kb = blockIdx.z * kg_per_split;
+    const int m0 = mtile * BM;
+    const int kb = split * kg_per_split;
     const int ke = min(KG, kb + kg_per_split);
-    const int tr = threadIdx.x >> 4;
-    const int tc = threadIdx.x & 15;
-    const u4_t* X4 = reinterpret_cast<const u4_t*>(x);
 
-    bool nok[NP];
-#pragma unroll
-    for (int p = 0; p < NP; ++p) nok[p] = ntw + p < NT;
+    const rsrc_t rw = make_rsrc(pw, (uint32_t)((size_t)K * N / 2));
+    const rsrc_t rs = make_rsrc(ps, (uint32_t)((size_t)K * N / 64));
+    const rsrc_t rz = make_rsrc(pz, (uint32_t)((size_t)K * N / 256));
+    const rsrc_t rx = make_rsrc(x, (uint32_t)((size_t)M * K * 2));
 
-    u4_t xr[XR];
-    auto load_x = [&](int kg) {
+    // weight units of this wave's n-tiles (clamped; out-of-range tiles are
+    // computed on valid data and never stored)
+    const int ntw = ntile * (4 * NP) + wave * NP;
+    uint32_t ubase[NP];
 #pragma unroll
-        for (int i = 0; i < XR; ++i) {
-            const int m = m0 + i * 16 + tr;
-            xr[i] = m < M ? X4[(size_t)m * KX + kg * 16 + tc] : u4_t{0u, 0u, 0u, 0u};
-        }
+    for (int p = 0; p < NP; ++p) ubase[p] = (uint32_t)min(ntw + p, NT - 1) * KG;
+    const uint32_t vw = lane * 16;
+    const uint32_t vs = c * 2;
+    const uint32_t vz = (c >> 3) * 4;
+
+    // LDS-DMA source offsets: this lane fills row rr of 1 KiB block i at chunk
+    // position (lane % 16), i.e. it fetches channel chunk (lane % 16) ^ (rr % 16).
+    uint32_t vx[DMA_PER_WAVE];
+#pragma unroll
+    for (int i = 0; i < DMA_PER_WAVE; ++i) {
+        const int rr = (wave * DMA_PER_WAVE + i) * 4 + (lane >> 4);
+        const int row = min(m0 + rr, M - 1);
+        vx[i] = (uint32_t)(row * K + 8 * ((lane & 15) ^ (rr & 15))) * 2;
+    }
+    auto dma_x = [&](int stage, int kg) {
+        // scalar operands by construction (the compiler may otherwise carry
+        // the loop counter in a VGPR and wrap each load in a waterfall loop)
+        const uint32_t soff = uniform((uint32_t)kg * 256u);
+#pragma unroll
+        for (int i = 0; i < DMA_PER_WAVE; ++i)
+            dma16(rx, lds + stage * STAGE + (wave * DMA_PER_WAVE + i) * 1024, vx[i], soff);
     };
-    auto store_x = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < XR; ++i) xs[buf][i * 16 + tr][tc] = xr[i];
-    };
 
-    u4_t wv[NP];
-    uint32_t sv[NP], zv[NP];
-    auto load_w = [&](u4_t* w, uint32_t* s, uint32_t* z, int kg) {
+    u4_t wr[2][NP];
+    uint32_t sr[2][NP], zr[2][NP];
+    auto load_w = [&](int r, int kg) {
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
-            const size_t unit = (size_t)(nok[p] ? ntw + p : 0) * KG + kg;
-            w[p] = nok[p] ? pw[unit * 64 + lane] : u4_t{0u, 0u, 0u, 0u};
-            s[p] = ps[unit * kUnitScales + c];
-            z[p] = pz[unit * kUnitZeroWords + (c >> 3)];
+            const uint32_t u = uniform(ubase[p] + kg);
+            wr[r][p] = ld128(rw, vw, u * 1024u);
+            sr[r][p] = ld16(rs, vs, u * 32u);
+            zr[r][p] = ld32(rz, vz, u * 8u);
         }
     };
 
@@ -311,53 +411,63 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 #pragma unroll
         for (int mt = 0; mt < MTT; ++mt) acc[p][mt] = f4_t{0.f, 0.f, 0.f, 0.f};
 
-    if (kb < ke) {
-        load_x(kb);
-        load_w(wv, sv, zv, kb);
-        store_x(0);
-    }
-    __syncthreads();
+    // fragment read offsets inside a stage: row mt*16 + c, chunk (4j+g) ^ c
+    auto bfrag = [&](int stage, int mt, int j) -> h8_t {
+        const uint8_t* src = lds + stage * STAGE + (mt * 16 + c) * ROWB + (((4 * j + g) ^ c) << 4);
+        return bits_as<h8_t>(*reinterpret_cast<const u4_t*>(src));
+    };
 
-    for (int kg = kb; kg < ke; ++kg) {
-        const int buf = (kg - kb) & 1;
-        const bool more = kg + 1 < ke;
-        u4_t wn[NP];
-        uint32_t sn[NP], zn[NP];
-        if (more) {
-            load_x(kg + 1);
-            load_w(wn, sn, zn, kg + 1);
-        }
+    auto kgroup = [&](int r, int stage) {
         Deq d[NP];
 #pragma unroll
-        for (int p = 0; p < NP; ++p) d[p] = make_deq(sv[p], (zv[p] >> (4 * (c & 7))) & 15u);
+        for (int p = 0; p < NP; ++p) d[p] = make_deq(sr[r][p], (zr[r][p] >> (4 * (c & 7))) & 15u);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             h8_t a[NP];
 #pragma unroll
-            for (int p = 0; p < NP; ++p) a[p] = dequant8(wv[p][j], d[p]);
+            for (int p = 0; p < NP; ++p) a[p] = dequant8(wr[r][p][j], d[p]);
 #pragma unroll
             for (int mt = 0; mt < MTT; ++mt) {
-                const h8_t b = bits_as<h8_t>(xs[buf][mt * 16 + c][j * 4 + g]);
+                const h8_t b = bfrag(stage, mt, j);
 #pragma unroll
                 for (int p = 0; p < NP; ++p) acc[p][mt] = mfma16(a[p], b, acc[p][mt]);
             }
+            // keep the scheduler from hoisting later steps' fragment reads
+            // (register pressure) across this point
+            sched_fence();
         }
-        if (more) {
-            store_x(buf ^ 1);
-#pragma unroll
-            for (int p = 0; p < NP; ++p) {
-                wv[p] = wn[p];
-                sv[p] = sn[p];
-                zv[p] = zn[p];
-            }
+    };
+
+    if (kb < ke) {
+        dma_x(0, kb);
+        load_w(0, kb);
+    }
+    wait_all();
+    __syncthreads();
+
+    // two k-groups per trip so the ring and stage indices are compile-time
+    for (int kg = kb; kg < ke; kg += 2) {
+        if (kg + 1 < ke) {
+            dma_x(1, kg + 1);
+            load_w(1, kg + 1);
         }
+        kgroup(0, 0);
+        wait_all();
+        __syncthreads();
+        if (kg + 1 >= ke) break;
+        if (kg + 2 < ke) {
+            dma_x(0, kg + 2);
+            load_w(0, kg + 2);
+        }
+        kgroup(1, 1);
+        wait_all();
         __syncthreads();
     }
 
-    if (gridDim.z == 1) {
+    if (n_splits == 1) {
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
-            if (!nok[p]) continue;
+            if (ntw + p >= NT) continue;
             const int n = (ntw + p) * 16 + 4 * g;
 #pragma unroll
             for (int mt = 0; mt < MTT; ++mt) {
@@ -366,10 +476,10 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
             }
         }
     } else {
-        float* part = ws + (size_t)blockIdx.z * M * N;
+        float* part = ws + (size_t)split * M * N;
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
-            if (!nok[p]) continue;
+            if (ntw + p >= NT) continue;
             const int n = (ntw + p) * 16 + 4 * g;
 #pragma unroll
             for (int mt = 0; mt < MTT; ++mt) {
@@ -541,8 +651,11 @@ void launch_stream_t(const uint16_t* x, const u4_t* pw, const uint16_t* ps, cons
 {
     const int NT = N / 16;
     dim3 grid((NT + NPW - 1) / NPW);
-    hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES>), grid, dim3(64 * WAVES), 0, st, x, pw, ps, pz,
-                       y, M, N, K);
+    // Ring depth: more k-groups in flight where the activation fragments
+    // leave registers for it.
+    constexpr int D = MT == 1 ? 4 : 2;
+    hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D>), grid, dim3(64 * WAVES), 0, st, x, pw, ps,
+                       pz, y, M, N, K);
 }
 
 template <int MT, int NPW>
@@ -585,9 +698,15 @@ template <int BM, int WN>
 void launch_tiled_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
                     const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st)
 {
-    dim3 grid(ceil_div(N, 4 * WN), ceil_div(M, BM), pl.split);
-    hipLaunchKernelGGL((tiled_kernel<BM, WN>), grid, dim3(256), 0, st, x, pw, ps, pz, y, ws, M, N, K,
-                       pl.kgps);
+    const int nm = ceil_div(M, BM);
+    const int nn = ceil_div(N, 4 * WN);
+    const int nblk = nm * nn * pl.split;
+    const int grid = ceil_div(nblk, 8) * 8;
+    // Two workgroups per CU (2 waves per SIMD, 256 registers per lane) where
+    // the tile's accumulators leave room for it; otherwise one (512).
+    constexpr int MINW = (BM * WN <= 128 * 32) ? 2 : 1;
+    hipLaunchKernelGGL((tiled_kernel<BM, WN, MINW>), dim3(grid), dim3(256), 0, st, x, pw, ps, pz, y, ws, M,
+                       N, K, pl.kgps, nm, nn, pl.split);
 }
 
 int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
@@ -617,7 +736,10 @@ int validate(const void* x, const void* packed, const void* scales, const void* 
     if (M < 0 || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return QUICK_ERR_SHAPE;
     // 32-bit index arithmetic inside the kernels: keep every operand well
     // inside the range (largest: packed words K*N/8, activations M*K).
-    if (K * N / 8 > ((int64_t)1 << 31) || M * K > ((int64_t)1 << 31) || M * N > ((int64_t)1 << 31) ||
+    // 32-bit buffer offsets and index arithmetic inside the kernels: packed
+    // weights (K*N/2 bytes) and activations (2*M*K bytes) below 4 GiB, the
+    // output below 2^31 elements.
+    if (K * N / 2 >= ((int64_t)1 << 32) || M * K >= ((int64_t)1 << 31) || M * N >= ((int64_t)1 << 31) ||
         M > (1 << 24))
         return QUICK_ERR_SHAPE;
     if (M == 0) return QUICK_OK;
