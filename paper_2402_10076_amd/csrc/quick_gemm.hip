@@ -143,6 +143,12 @@ __device__ __forceinline__ void dma16(rsrc_t r, void* dst, uint32_t voff, uint32
 }
 // Wait until every outstanding memory operation of this wave has completed.
 __device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0); }
+// Workgroup execution barrier without memory-fence semantics.  Used where
+// explicit counter waits already order the memory traffic: every LDS-DMA a
+// wave issued for the next stage has completed (its vmcnt wait) and every LDS
+// read of the stage about to be overwritten has returned (its data fed the
+// matrix instructions before the barrier).
+__device__ __forceinline__ void barrier() { __builtin_amdgcn_s_barrier(); }
 // Scheduling fence: no instruction moves across it.
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 __device__ __forceinline__ uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -301,45 +307,69 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 // ---------------------------------------------------------------------------
 // Tiled kernel (large M, matrix-core-bound).
 //
-// A workgroup of 4 waves computes a BM x (4*WN) output tile; the waves split
-// the columns (each wave WN columns and all BM rows), so every packed weight
-// is loaded and dequantized exactly once per workgroup, straight into VGPRs
-// (Section 3.1), and the only LDS traffic is the activation tile
-// (Section 3.3: LDS holds activations only, which leaves room for big tiles).
+// One workgroup of WAVES waves per CU computes a BM x (WAVES*WN) output tile;
+// the waves split the columns (each wave WN columns and all BM rows), so
+// every packed weight is loaded and dequantized exactly once per workgroup,
+// straight into VGPRs (Section 3.1), and the activation tile in LDS is shared
+// by all of them (Section 3.3: LDS holds activations only, which leaves room
+// for a big tile and a deep ring).
 //
-// Activation tile: BM rows x 128 input channels (one k-group) per stage, two
-// stages.  It is copied global -> LDS by the 16-byte LDS-DMA form of the
-// buffer load (no staging registers): one instruction moves 4 rows, lane L
-// landing at byte 16*L of the instruction's 1 KiB.  Inside a 256-byte row the
-// 16-byte chunk holding channels 8*q .. 8*q+7 sits at position q ^ (row % 16),
-// so the fragment reads of 16 consecutive rows at one chunk index hit 16
-// distinct bank groups.
+// Activations: a ring of NST LDS stages of BM rows x 128 input channels (one
+// k-group).  Each stage is filled global -> LDS by the 16-byte LDS-DMA form of
+// the buffer load (no staging registers): one instruction moves 4 rows, lane
+// L landing at byte 16*L of the instruction's 1 KiB.  Inside a 256-byte row
+// the 16-byte chunk holding channels 8*q .. 8*q+7 sits at position
+// q ^ (row % 16), so fragment reads of 16 consecutive rows at one chunk index
+// hit 16 distinct bank groups.
 //
-// Weights: one 16-byte load per lane and n-tile per k-group, into a
-// two-stage register ring filled one k-group ahead.  Within a k-group the
-// dequantization of step j+1 is issued between the matrix instructions of
-// step j by the scheduler (two waves per SIMD where registers allow).
+// Weights: one 16-byte load per lane and n-tile per k-group into a ring of
+// NST register slots.  k-group k+NST-1 (activations and weights) is requested
+// while k-group k is computed; the end-of-k-group wait only drains the loads
+// of k-group k+1 (vector-memory counters retire in issue order), so NST-2
+// k-groups stay in flight across the barrier.
+//
+// Inside a k-group: 4 steps of 32 channels, software-pipelined -- while the
+// matrix instructions of step j run, the activation fragments of step j+1
+// are read from LDS and the weights of step j+1 are dequantized.
 //
 // Tiles are numbered M-fastest and assigned so that consecutive numbers run
-// on the same XCD (hardware hands workgroup ids to the 8 XCDs round-robin):
-// the M-tiles sharing an N-tile's weights then share one L2.
-// gridDim.x > tiles*splits pads to a multiple of 8; those workgroups exit.
-// With splits > 1 each split writes fp32 partial sums to the workspace and a
-// second kernel adds them in split order.
+// on the same XCD (workgroup ids go to the 8 XCDs round-robin): M-tiles that
+// share an N-tile's weights share one L2.  gridDim.x is padded to a multiple
+// of 8; the extra workgroups exit at once.  With splits > 1 each split writes
+// fp32 partial sums to the workspace and a second kernel adds them in split
+// order.
 // ---------------------------------------------------------------------------
-template <int BM, int WN, int MINW>
-__global__ void __launch_bounds__(256, MINW)
+constexpr int kTiledWaves = 8;
+constexpr int kTiledStages = 4;
+
+template <int BM, int WN>
+__global__ void __launch_bounds__(64 * kTiledWaves, 1)
 tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
              const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
              uint16_t* __restrict__ y, float* __restrict__ ws, int M, int N, int K,
              int kg_per_split, int n_mtiles, int n_ntiles, int n_splits)
 {
-    constexpr int NP = WN / 16;         // n-tiles per wave
-    constexpr int MTT = BM / 16;        // 16-row blocks per workgroup
-    constexpr int ROWB = 256;           // bytes per activation row of a stage
-    constexpr int STAGE = BM * ROWB;    // bytes per stage
-    constexpr int DMA_PER_WAVE = BM / 16;  // 1 KiB LDS-DMA instructions per wave and stage
-    __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * STAGE];
+    constexpr int WAVES = kTiledWaves;
+    constexpr int NST = kTiledStages;
+    constexpr int NP = WN / 16;                   // n-tiles per wave
+    constexpr int MTT = BM / 16;                  // 16-row blocks
+    constexpr int ROWB = 256;                     // bytes per activation row of a stage
+    constexpr int STAGE = BM * ROWB;              // bytes per stage
+    constexpr int DMA_PER_WAVE = STAGE / 1024 / WAVES;
+    constexpr int GROUP_LOADS = DMA_PER_WAVE + 3 * NP;  // vector-memory ops per k-group and wave
+    static_assert(DMA_PER_WAVE >= 1 && STAGE % (1024 * WAVES) == 0, "stage must split into 1 KiB per wave");
+    static_assert(2 * GROUP_LOADS < 64, "vmcnt range");
+    // one LDS object per stage: the compiler can then tell that a DMA into
+    // one stage does not alias fragment reads from another, and does not
+    // drain in-flight DMAs before every read
+    static_assert(NST == 4, "stage objects below");
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_s0[STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_s1[STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_s2[STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_s3[STAGE];
+    auto stage_ptr = [&](int st) -> uint8_t* {
+        return st == 0 ? lds_s0 : st == 1 ? lds_s1 : st == 2 ? lds_s2 : lds_s3;
+    };
 
     // ---- tile assignment (XCD-aware, M-fastest)
     const int nblk = n_mtiles * n_ntiles * n_splits;
@@ -367,7 +397,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 
     // weight units of this wave's n-tiles (clamped; out-of-range tiles are
     // computed on valid data and never stored)
-    const int ntw = ntile * (4 * NP) + wave * NP;
+    const int ntw = ntile * (WAVES * NP) + wave * NP;
     uint32_t ubase[NP];
 #pragma unroll
     for (int p = 0; p < NP; ++p) ubase[p] = (uint32_t)min(ntw + p, NT - 1) * KG;
@@ -384,25 +414,28 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         const int row = min(m0 + rr, M - 1);
         vx[i] = (uint32_t)(row * K + 8 * ((lane & 15) ^ (rr & 15))) * 2;
     }
-    auto dma_x = [&](int stage, int kg) {
-        // scalar operands by construction (the compiler may otherwise carry
-        // the loop counter in a VGPR and wrap each load in a waterfall loop)
+
+    u4_t wr[NST][NP];
+    uint32_t sr[NST][NP], zr[NST][NP];
+    // k-group kg's activations -> LDS stage st and weights -> ring slot st
+    auto fetch = [&](int st, int kg) {
         const uint32_t soff = uniform((uint32_t)kg * 256u);
 #pragma unroll
         for (int i = 0; i < DMA_PER_WAVE; ++i)
-            dma16(rx, lds + stage * STAGE + (wave * DMA_PER_WAVE + i) * 1024, vx[i], soff);
-    };
-
-    u4_t wr[2][NP];
-    uint32_t sr[2][NP], zr[2][NP];
-    auto load_w = [&](int r, int kg) {
+            dma16(rx, stage_ptr(st) + (wave * DMA_PER_WAVE + i) * 1024, vx[i], soff);
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
             const uint32_t u = uniform(ubase[p] + kg);
-            wr[r][p] = ld128(rw, vw, u * 1024u);
-            sr[r][p] = ld16(rs, vs, u * 32u);
-            zr[r][p] = ld32(rz, vz, u * 8u);
+            wr[st][p] = ld128(rw, vw, u * 1024u);
+            sr[st][p] = ld16(rs, vs, u * 32u);
+            zr[st][p] = ld32(rz, vz, u * 8u);
         }
+    };
+    // wait until at most `groups` k-groups of loads are still in flight
+    auto wait_groups = [&](int groups) {
+        if (groups >= 2) __builtin_amdgcn_s_waitcnt(0x0F70 | (2 * GROUP_LOADS & 15) | ((2 * GROUP_LOADS >> 4) << 14));
+        else if (groups == 1) __builtin_amdgcn_s_waitcnt(0x0F70 | (GROUP_LOADS & 15) | ((GROUP_LOADS >> 4) << 14));
+        else __builtin_amdgcn_s_waitcnt(0x0F70);
     };
 
     f4_t acc[NP][MTT];
@@ -411,57 +444,77 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 #pragma unroll
         for (int mt = 0; mt < MTT; ++mt) acc[p][mt] = f4_t{0.f, 0.f, 0.f, 0.f};
 
-    // fragment read offsets inside a stage: row mt*16 + c, chunk (4j+g) ^ c
-    auto bfrag = [&](int stage, int mt, int j) -> h8_t {
-        const uint8_t* src = lds + stage * STAGE + (mt * 16 + c) * ROWB + (((4 * j + g) ^ c) << 4);
+    // fragment read inside a stage: row mt*16 + c, chunk (4j+g) ^ c
+    auto bfrag = [&](int st, int mt, int j) -> h8_t {
+        const uint8_t* src = stage_ptr(st) + (mt * 16 + c) * ROWB + (((4 * j + g) ^ c) << 4);
         return bits_as<h8_t>(*reinterpret_cast<const u4_t*>(src));
     };
 
-    auto kgroup = [&](int r, int stage) {
+    auto kgroup = [&](int st) {
         Deq d[NP];
 #pragma unroll
-        for (int p = 0; p < NP; ++p) d[p] = make_deq(sr[r][p], (zr[r][p] >> (4 * (c & 7))) & 15u);
+        for (int p = 0; p < NP; ++p) d[p] = make_deq(sr[st][p], (zr[st][p] >> (4 * (c & 7))) & 15u);
+        h8_t a[2][NP];
+        h8_t b[2][MTT];
+#pragma unroll
+        for (int p = 0; p < NP; ++p) a[0][p] = dequant8(wr[st][p][0], d[p]);
+#pragma unroll
+        for (int mt = 0; mt < MTT; ++mt) b[0][mt] = bfrag(st, mt, 0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            h8_t a[NP];
-#pragma unroll
-            for (int p = 0; p < NP; ++p) a[p] = dequant8(wr[r][p][j], d[p]);
+            const int cu = j & 1, nx = cu ^ 1;
 #pragma unroll
             for (int mt = 0; mt < MTT; ++mt) {
-                const h8_t b = bfrag(stage, mt, j);
 #pragma unroll
-                for (int p = 0; p < NP; ++p) acc[p][mt] = mfma16(a[p], b, acc[p][mt]);
+                for (int p = 0; p < NP; ++p) acc[p][mt] = mfma16(a[cu][p], b[cu][mt], acc[p][mt]);
+                if (j < 3) b[nx][mt] = bfrag(st, mt, j + 1);
             }
-            // keep the scheduler from hoisting later steps' fragment reads
-            // (register pressure) across this point
-            sched_fence();
+            if (j < 3) {
+#pragma unroll
+                for (int p = 0; p < NP; ++p) a[nx][p] = dequant8(wr[st][p][j + 1], d[p]);
+                constexpr int VPER = (13 * NP + MTT - 1) / MTT;  // dequant VALU ops per block
+#pragma unroll
+                for (int mt = 0; mt < MTT; ++mt) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, NP, 0);   // matrix
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // LDS read
+                    __builtin_amdgcn_sched_group_barrier(0x002, VPER, 0); // VALU
+                }
+            }
         }
     };
 
-    if (kb < ke) {
-        dma_x(0, kb);
-        load_w(0, kb);
-    }
-    wait_all();
-    __syncthreads();
+    // prologue: k-groups kb .. kb+NST-2 in flight, then wait for kb
+#pragma unroll
+    for (int i = 0; i < NST - 1; ++i)
+        if (kb + i < ke) fetch(i, kb + i);
+    wait_groups(min(NST - 2, ke - kb - 1));
+    barrier();
 
-    // two k-groups per trip so the ring and stage indices are compile-time
-    for (int kg = kb; kg < ke; kg += 2) {
-        if (kg + 1 < ke) {
-            dma_x(1, kg + 1);
-            load_w(1, kg + 1);
+    // steady state: straight-line body (unconditional requests) so the
+    // compiler's own wait analysis keeps the requested k-groups in flight
+    int kg = kb;
+    for (; kg + 2 * NST - 1 <= ke; kg += NST) {
+#pragma unroll
+        for (int i = 0; i < NST; ++i) {
+            fetch((i + NST - 1) % NST, kg + i + NST - 1);
+            kgroup(i);
+            // k-group kg+i+1 must have landed; later ones stay in flight
+            wait_groups(NST - 2);
+            barrier();
         }
-        kgroup(0, 0);
-        wait_all();
-        __syncthreads();
-        if (kg + 1 >= ke) break;
-        if (kg + 2 < ke) {
-            dma_x(0, kg + 2);
-            load_w(0, kg + 2);
+    }
+    // tail
+    for (; kg < ke; kg += NST) {
+#pragma unroll
+        for (int i = 0; i < NST; ++i) {
+            const int k = kg + i;
+            if (k < ke) {
+                if (k + NST - 1 < ke) fetch((i + NST - 1) % NST, k + NST - 1);
+                kgroup(i);
+                wait_groups(min(NST - 2, ke - k - 2));
+                barrier();
+            }
         }
-        kgroup(1, 1);
-        wait_all();
-        __syncthreads();
     }
 
     if (n_splits == 1) {
@@ -533,16 +586,23 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
         pl->bm = 0;
         pl->kgps = 0;
     } else {
+        // one 8-wave workgroup per CU computes BM x 256; split K until the
+        // tiles (times splits) cover the 256 CUs, keeping >= 8 k-groups per split
         pl->variant = kVariantTiled;
         pl->bm = M <= 96 ? 64 : 128;
-        pl->wn = 64;
-        const int64_t tiles = (int64_t)ceil_div(M, pl->bm) * ceil_div(N, 4 * pl->wn);
+        pl->wn = 32;
+        const int64_t tiles = (int64_t)ceil_div(M, pl->bm) * ceil_div(N, kTiledWaves * pl->wn);
         int s = 1;
-        while (tiles * s < 256 && KG / (2 * s) >= 4) s *= 2;
+        while (tiles * s < 256 && KG / (2 * s) >= 8 && s < 8) s *= 2;
         pl->split = s;
         pl->kgps = 0;
     }
     return QUICK_OK;
+}
+
+bool tiled_supported(int bm, int wn)
+{
+    return (bm == 64 && wn == 32) || (bm == 128 && wn == 32) || (bm == 64 && wn == 64);
 }
 
 int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* pl)
@@ -568,7 +628,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
         if (pl->variant != kVariantTiled) {
             pl->variant = kVariantTiled;
             pl->bm = 64;
-            pl->wn = 64;
+            pl->wn = 32;
             pl->split = 1;
         }
     }
@@ -585,8 +645,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
             if (cfg->split_k > KG) return QUICK_ERR_INVALID_ARG;
             pl->split = cfg->split_k;
         }
-        // 256 x 64-column waves need more than 512 registers per lane.
-        if (pl->bm == 256 && pl->wn == 64) return QUICK_ERR_INVALID_ARG;
+        if (!tiled_supported(pl->bm, pl->wn)) return QUICK_ERR_INVALID_ARG;
     }
     return QUICK_OK;
 }
@@ -699,24 +758,19 @@ void launch_tiled_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uin
                     const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st)
 {
     const int nm = ceil_div(M, BM);
-    const int nn = ceil_div(N, 4 * WN);
+    const int nn = ceil_div(N, kTiledWaves * WN);
     const int nblk = nm * nn * pl.split;
     const int grid = ceil_div(nblk, 8) * 8;
-    // Two workgroups per CU (2 waves per SIMD, 256 registers per lane) where
-    // the tile's accumulators leave room for it; otherwise one (512).
-    constexpr int MINW = (BM * WN <= 128 * 32) ? 2 : 1;
-    hipLaunchKernelGGL((tiled_kernel<BM, WN, MINW>), dim3(grid), dim3(256), 0, st, x, pw, ps, pz, y, ws, M,
-                       N, K, pl.kgps, nm, nn, pl.split);
+    hipLaunchKernelGGL((tiled_kernel<BM, WN>), dim3(grid), dim3(64 * kTiledWaves), 0, st, x, pw, ps, pz, y,
+                       ws, M, N, K, pl.kgps, nm, nn, pl.split);
 }
 
 int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
                  const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st)
 {
     if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
-    else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
     else if (pl.bm == 128 && pl.wn == 32) launch_tiled_t<128, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
-    else if (pl.bm == 128 && pl.wn == 64) launch_tiled_t<128, 64>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
-    else if (pl.bm == 256 && pl.wn == 32) launch_tiled_t<256, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
+    else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
     else return QUICK_ERR_INVALID_ARG;
     if (pl.split > 1) {
         const int64_t MN = (int64_t)M * N;

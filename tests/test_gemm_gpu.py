@@ -21,7 +21,7 @@ pytestmark = pytest.mark.gpu
 
 STREAM_CFGS = [dict(variant=1, split_k=w, tile_n=p) for w in (1, 2, 4, 8) for p in (1, 2)]
 TILED_CFGS = [dict(variant=2, tile_m=bm, tile_n=wn, split_k=s)
-              for bm, wn in ((64, 32), (64, 64), (128, 32), (128, 64), (256, 32)) for s in (1, 3)]
+              for bm, wn in ((64, 32), (64, 64), (128, 32)) for s in (1, 3)]
 
 
 def _check(M, K, N, cfg, seed):
@@ -64,7 +64,7 @@ def test_c1_toy_full_output():
 
 
 @pytest.mark.parametrize("cfg", [None, dict(variant=1, split_k=4, tile_n=2), dict(variant=2, tile_m=64, tile_n=32, split_k=2),
-                                 dict(variant=2, tile_m=128, tile_n=64, split_k=1)])
+                                 dict(variant=2, tile_m=128, tile_n=32, split_k=1)])
 def test_one_hot_rows_give_exact_dequant(cfg):
     """x row m = e_{k_m}: y[m][n] is a single product, so it must equal the
     binary16 rounding of (q - z) * s exactly."""
