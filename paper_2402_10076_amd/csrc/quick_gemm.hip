@@ -586,14 +586,16 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
         pl->bm = 0;
         pl->kgps = 0;
     } else {
-        // one 8-wave workgroup per CU computes BM x 256; split K until the
-        // tiles (times splits) cover the 256 CUs, keeping >= 8 k-groups per split
+        // one 8-wave workgroup per CU computes BM x 256; split K while the
+        // tiles (times splits) leave well over a third of the 256 CUs idle
+        // (the partial-sum pass costs more than a partly idle chip above
+        // that), keeping >= 8 k-groups per split
         pl->variant = kVariantTiled;
         pl->bm = M <= 96 ? 64 : 128;
         pl->wn = 32;
         const int64_t tiles = (int64_t)ceil_div(M, pl->bm) * ceil_div(N, kTiledWaves * pl->wn);
         int s = 1;
-        while (tiles * s < 256 && KG / (2 * s) >= 8 && s < 8) s *= 2;
+        while (tiles * s < 160 && KG / (2 * s) >= 8 && s < 8) s *= 2;
         pl->split = s;
         pl->kgps = 0;
     }
