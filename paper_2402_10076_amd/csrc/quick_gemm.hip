@@ -31,6 +31,7 @@
 #include <cstring>
 #include <map>
 #include <mutex>
+#include <type_traits>
 #include <utility>
 
 #include "quick.h"
@@ -162,15 +163,31 @@ __device__ __forceinline__ uint32_t ld16(rsrc_t r, uint32_t voff, uint32_t soff)
 // Stream kernel (small M, bandwidth-bound).
 //
 // A workgroup owns NPW n-tiles (16 columns each) and the whole K range; its
-// WAVES waves split the k-groups between them (in-workgroup split-K).  Each
-// wave streams its packed units from HBM with one 16-byte load per lane and
-// unit through a ring of D register stages, so D k-groups of weights are in
-// flight while one is dequantized and multiplied.  Activation fragments (MT
-// blocks of 16 rows) are read from global memory one k-group ahead (they are
-// small and shared by every workgroup, so they hit in cache).  At the end the
-// waves' fp32 partial tiles are summed through LDS in wave order
-// (deterministic) and stored.
+// WAVES waves split the k-groups between them (in-workgroup split-K, no
+// partial sums leave the workgroup).  Each wave streams its packed units from
+// HBM with one 16-byte load per lane and unit through a ring of D register
+// stages, so D k-groups of weights are in flight while one is dequantized and
+// multiplied.  At the end the waves' fp32 partial tiles are summed through
+// LDS in wave order (deterministic) and stored.
+//
+// Activation fragments (B operand, MT blocks of 16 rows):
+//  * XL: the wave first copies its own k-range of all M rows of x into its
+//    slice of LDS with the 16-byte LDS-DMA load (rows contiguous, row stride
+//    = the slice width), waits for it, and then reads fragments with LDS
+//    reads; lanes of rows >= M read row M-1 (broadcast).  No barrier: a wave
+//    only reads what it copied.  Used when all of x fits (M*K*2 bytes).
+//  * otherwise the fragments are 16-byte buffer loads from global memory
+//    (they are small and shared by every workgroup, so they hit in cache),
+//    one k-group ahead.
 // ---------------------------------------------------------------------------
+// Per-wave LDS slice of the stream kernel's staged activations: M rows of
+// the wave's k-range (at most ceil(KG/WAVES) k-groups of 256 bytes per row),
+// rounded up to whole 1 KiB copy instructions.
+__host__ __device__ constexpr uint32_t stream_slice_bytes(int M, int KG, int WAVES)
+{
+    return (uint32_t)((M * ((KG + WAVES - 1) / WAVES) * 256 + 1023) / 1024 * 1024);
+}
+
 template <int NPW>
 struct WStage {
     u4_t w[NPW];
@@ -178,13 +195,14 @@ struct WStage {
     uint32_t z[NPW];
 };
 
-template <int MT, int NPW, int WAVES, int D>
+template <int MT, int NPW, int WAVES, int D, bool XL>
 __global__ void __launch_bounds__(64 * WAVES)
 stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
               const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
               uint16_t* __restrict__ y, int M, int N, int K)
 {
     static_assert(D % 2 == 0, "ring depth must be even (activation double buffer parity)");
+    extern __shared__ __attribute__((aligned(16))) uint8_t xlds[];
     const int KG = K >> 7;
     const int NT = N >> 4;
     const int lane = threadIdx.x & 63;
@@ -196,6 +214,7 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     const int nt0 = blockIdx.x * NPW;
     const int kb = (KG * wave) / WAVES;
     const int ke = (KG * (wave + 1)) / WAVES;
+    const int nk = ke - kb;
 
     const rsrc_t rw = make_rsrc(pw, (uint32_t)((size_t)K * N / 2));
     const rsrc_t rs = make_rsrc(ps, (uint32_t)((size_t)K * N / 64));
@@ -212,9 +231,36 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     const uint32_t vw = lane * 16;
     const uint32_t vs = c * 2;
     const uint32_t vz = (c >> 3) * 4;
+
+    // activation fragment source per 16-row block: global byte offset of
+    // (row, channel 8*g) [global path] or LDS offset inside the wave's slice
+    // [XL path]
     uint32_t vx[MT];
+    // this wave's slice: M rows x nk*256 bytes, at a fixed per-wave stride
+    // that is a 1 KiB multiple, so the last copy instruction's extra lanes
+    // stay inside the wave's own slice
+    uint8_t* xslice = xlds + (size_t)wave * stream_slice_bytes(M, KG, WAVES);
+    const uint32_t xrow = (uint32_t)nk * 256;         // slice row stride
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt) vx[mt] = (uint32_t)(min(mt * 16 + c, M - 1) * K + g * 8) * 2;
+    for (int mt = 0; mt < MT; ++mt) {
+        const int row = min(mt * 16 + c, M - 1);
+        vx[mt] = XL ? (uint32_t)(row * xrow + g * 16) : (uint32_t)(row * K + g * 8) * 2;
+    }
+
+    if constexpr (XL) {
+        // copy rows 0..M-1, channels kb*128 .. ke*128 into the slice: 16 bytes
+        // per lane, slice byte b = row*xrow + q*16 <- x[row][kb*128 + 8q ..]
+        const int chunks = M * nk * 16;   // 16-byte chunks in the slice
+        for (int i0 = 0; i0 < chunks; i0 += 64) {
+            const int idx = min(i0 + lane, chunks - 1);
+            const int row = idx / (nk * 16);
+            const int q = idx - row * nk * 16;
+            const uint32_t src = (uint32_t)(row * K + kb * 128 + q * 8) * 2;
+            // the last instruction may have fewer than 64 chunks: its extra
+            // lanes repeat the final chunk into the slice's padding
+            dma16(rx, xslice + (size_t)i0 * 16, src, 0);
+        }
+    }
 
     f4_t acc[NPW][MT];
 #pragma unroll
@@ -228,17 +274,26 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     auto load_w = [&](WStage<NPW>& st, int kg) {
 #pragma unroll
         for (int p = 0; p < NPW; ++p) {
-            const uint32_t u = ubase[p] + kg;
+            const uint32_t u = uniform(ubase[p] + kg);
             st.w[p] = ld128(rw, vw, u * 1024u);
             st.s[p] = ld16(rs, vs, u * 32u);
             st.z[p] = ld32(rz, vz, u * 8u);
         }
     };
     auto load_x = [&](u4_t (&xb)[MT][4], int kg) {
+        if constexpr (XL) {
+            const int kl = kg - kb;
 #pragma unroll
-        for (int mt = 0; mt < MT; ++mt)
+            for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) xb[mt][j] = ld128(rx, vx[mt] + j * 64, kg * 256u);
+                for (int j = 0; j < 4; ++j)
+                    xb[mt][j] = *reinterpret_cast<const u4_t*>(xslice + vx[mt] + kl * 256 + j * 64);
+        } else {
+#pragma unroll
+            for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) xb[mt][j] = ld128(rx, vx[mt] + j * 64, uniform(kg * 256u));
+        }
     };
     auto compute = [&](const WStage<NPW>& st, const u4_t (&xb)[MT][4]) {
         Deq d[NPW];
@@ -259,9 +314,27 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 #pragma unroll
     for (int i = 0; i < D; ++i)
         if (kb + i < ke) load_w(ring[i], kb + i);
+    if constexpr (XL) wait_all();  // the slice has landed (weights too, once)
     if (kb < ke) load_x(xf[0], kb);
 
-    for (int kg = kb; kg < ke; kg += D) {
+    // steady state: straight-line body with unconditional requests, so the
+    // compiler's wait analysis keeps D-1 stages in flight instead of
+    // draining the ring at every trip
+    int kg = kb;
+    for (; kg + 2 * D <= ke; kg += D) {
+#pragma unroll
+        for (int i = 0; i < D; ++i) {
+            load_x(xf[(i + 1) & 1], kg + i + 1);
+            compute(ring[i], xf[i & 1]);
+            load_w(ring[i], kg + i + D);
+            // keep each refill where it is: the scheduler would otherwise
+            // sink all of them to the end of the trip and issue them in one
+            // burst that the next trip then waits for
+            sched_fence();
+        }
+    }
+    // tail
+    for (; kg < ke; kg += D) {
 #pragma unroll
         for (int i = 0; i < D; ++i) {
             const int k = kg + i;
@@ -355,10 +428,12 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     constexpr int MTT = BM / 16;                  // 16-row blocks
     constexpr int ROWB = 256;                     // bytes per activation row of a stage
     constexpr int STAGE = BM * ROWB;              // bytes per stage
-    constexpr int DMA_PER_WAVE = STAGE / 1024 / WAVES;
-    constexpr int GROUP_LOADS = DMA_PER_WAVE + 3 * NP;  // vector-memory ops per k-group and wave
-    static_assert(DMA_PER_WAVE >= 1 && STAGE % (1024 * WAVES) == 0, "stage must split into 1 KiB per wave");
-    static_assert(2 * GROUP_LOADS < 64, "vmcnt range");
+    // 1 KiB LDS-DMA instructions per stage; wave w issues instructions
+    // w, w + WAVES, ...  (for BM = 16 only waves 0..3 have one)
+    constexpr int NDMA = STAGE / 1024;
+    constexpr int DMA_PER_WAVE = (NDMA + WAVES - 1) / WAVES;   // upper bound per wave
+    static_assert(NDMA >= 1 && STAGE % 1024 == 0 && (NDMA % WAVES == 0 || NDMA < WAVES), "DMA split");
+    static_assert(2 * (DMA_PER_WAVE + 3 * NP) < 64, "vmcnt range");
     // one LDS object per stage: the compiler can then tell that a DMA into
     // one stage does not alias fragment reads from another, and does not
     // drain in-flight DMAs before every read
@@ -407,10 +482,12 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 
     // LDS-DMA source offsets: this lane fills row rr of 1 KiB block i at chunk
     // position (lane % 16), i.e. it fetches channel chunk (lane % 16) ^ (rr % 16).
+    // this wave's DMA instruction count (wave-uniform)
+    const int ndma = NDMA >= WAVES ? DMA_PER_WAVE : (wave < NDMA ? 1 : 0);
     uint32_t vx[DMA_PER_WAVE];
 #pragma unroll
     for (int i = 0; i < DMA_PER_WAVE; ++i) {
-        const int rr = (wave * DMA_PER_WAVE + i) * 4 + (lane >> 4);
+        const int rr = (wave + i * WAVES) * 4 + (lane >> 4);
         const int row = min(m0 + rr, M - 1);
         vx[i] = (uint32_t)(row * K + 8 * ((lane & 15) ^ (rr & 15))) * 2;
     }
@@ -422,7 +499,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         const uint32_t soff = uniform((uint32_t)kg * 256u);
 #pragma unroll
         for (int i = 0; i < DMA_PER_WAVE; ++i)
-            dma16(rx, stage_ptr(st) + (wave * DMA_PER_WAVE + i) * 1024, vx[i], soff);
+            if (i < ndma) dma16(rx, stage_ptr(st) + (wave + i * WAVES) * 1024, vx[i], soff);
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
             const uint32_t u = uniform(ubase[p] + kg);
@@ -432,10 +509,21 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         }
     };
     // wait until at most `groups` k-groups of loads are still in flight
+    // s_waitcnt immediate (gfx9): vmcnt in bits 3:0 and 15:14, expcnt 6:4 and
+    // lgkmcnt 11:8 left at their maxima (no wait)
+    auto wait_vm = [](auto n) { __builtin_amdgcn_s_waitcnt(0x0F70 | (n & 15) | ((n >> 4) << 14)); };
+    constexpr int GL_FULL = DMA_PER_WAVE + 3 * NP;      // loads per k-group, waves with DMA
+    constexpr int GL_NODMA = 3 * NP;                    // waves without (BM = 16, waves 4..7)
     auto wait_groups = [&](int groups) {
-        if (groups >= 2) __builtin_amdgcn_s_waitcnt(0x0F70 | (2 * GROUP_LOADS & 15) | ((2 * GROUP_LOADS >> 4) << 14));
-        else if (groups == 1) __builtin_amdgcn_s_waitcnt(0x0F70 | (GROUP_LOADS & 15) | ((GROUP_LOADS >> 4) << 14));
-        else __builtin_amdgcn_s_waitcnt(0x0F70);
+        if (ndma == DMA_PER_WAVE) {
+            if (groups >= 2) wait_vm(std::integral_constant<int, 2 * GL_FULL>{});
+            else if (groups == 1) wait_vm(std::integral_constant<int, GL_FULL>{});
+            else wait_vm(std::integral_constant<int, 0>{});
+        } else {
+            if (groups >= 2) wait_vm(std::integral_constant<int, 2 * GL_NODMA>{});
+            else if (groups == 1) wait_vm(std::integral_constant<int, GL_NODMA>{});
+            else wait_vm(std::integral_constant<int, 0>{});
+        }
     };
 
     f4_t acc[NP][MTT];
@@ -560,6 +648,7 @@ splitk_reduce_kernel(const float* __restrict__ ws, uint16_t* __restrict__ y, int
 // Host side: validation, configuration, workspace, launch.
 // ---------------------------------------------------------------------------
 constexpr int kVariantStream = 1;
+constexpr size_t kStreamLdsX = 64 * 1024;  // LDS bytes the stream kernel may give to activations
 constexpr int kVariantTiled = 2;
 
 struct Plan {
@@ -576,7 +665,7 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
 {
     const int64_t KG = K / 128;
     const int64_t NT = N / 16;
-    if (M <= 64) {
+    auto stream_plan = [&]() {
         pl->variant = kVariantStream;
         pl->wn = NT / 2 >= 512 ? 2 : 1;
         const int64_t wgs = (NT + pl->wn - 1) / pl->wn;
@@ -585,26 +674,52 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
         pl->split = w;
         pl->bm = 0;
         pl->kgps = 0;
-    } else {
-        // one 8-wave workgroup per CU computes BM x 256; split K while the
-        // tiles (times splits) leave well over a third of the 256 CUs idle
-        // (the partial-sum pass costs more than a partly idle chip above
-        // that), keeping >= 8 k-groups per split
-        pl->variant = kVariantTiled;
-        pl->bm = M <= 96 ? 64 : 128;
-        pl->wn = 32;
-        const int64_t tiles = (int64_t)ceil_div(M, pl->bm) * ceil_div(N, kTiledWaves * pl->wn);
-        int s = 1;
-        while (tiles * s < 160 && KG / (2 * s) >= 8 && s < 8) s *= 2;
-        pl->split = s;
-        pl->kgps = 0;
+    };
+    if (M <= 8) {
+        // weights dominate; each wave streams its own k-range (no LDS tile)
+        stream_plan();
+        return QUICK_OK;
     }
+    // Tiled kernel: an 8-wave workgroup computes BM x (8*WN), sharing one
+    // activation tile in LDS.  Small BM tiles fit several workgroups per CU,
+    // so they split K until ~384 workgroups exist; the 64/128-row tiles run
+    // one workgroup per CU and split only when fewer than 160 tiles exist.
+    pl->variant = kVariantTiled;
+    if (M <= 16) {
+        pl->bm = 16;
+        pl->wn = 16;
+    } else if (M <= 32) {
+        pl->bm = 32;
+        pl->wn = 16;
+    } else if (M <= 64) {
+        const bool wide = (int64_t)ceil_div(M, 64) * ceil_div(N, 256) >= 160;
+        pl->bm = wide ? 64 : 32;
+        pl->wn = wide ? 32 : 16;
+    } else if (M <= 96) {
+        pl->bm = 64;
+        pl->wn = 32;
+    } else {
+        pl->bm = 128;
+        pl->wn = 32;
+    }
+    const int64_t tiles = (int64_t)ceil_div(M, pl->bm) * ceil_div(N, kTiledWaves * pl->wn);
+    if (pl->bm == 16 && tiles < 48) {
+        // too few column tiles to feed the chip without heavy split-K
+        stream_plan();
+        return QUICK_OK;
+    }
+    const int64_t target = pl->wn == 16 ? 384 : 160;
+    int s = 1;
+    while (tiles * s < target && KG / (2 * s) >= 4 && s < 8) s *= 2;
+    pl->split = s;
+    pl->kgps = 0;
     return QUICK_OK;
 }
 
 bool tiled_supported(int bm, int wn)
 {
-    return (bm == 64 && wn == 32) || (bm == 128 && wn == 32) || (bm == 64 && wn == 64);
+    return ((bm == 16 || bm == 32) && (wn == 16 || wn == 32)) || (bm == 64 && wn == 32) ||
+           (bm == 128 && wn == 32) || (bm == 64 && wn == 64);
 }
 
 int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* pl)
@@ -636,11 +751,12 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
     }
     if (pl->variant == kVariantTiled) {
         if (cfg->tile_m) {
-            if (cfg->tile_m != 64 && cfg->tile_m != 128 && cfg->tile_m != 256) return QUICK_ERR_INVALID_ARG;
+            if (cfg->tile_m != 16 && cfg->tile_m != 32 && cfg->tile_m != 64 && cfg->tile_m != 128)
+                return QUICK_ERR_INVALID_ARG;
             pl->bm = cfg->tile_m;
         }
         if (cfg->tile_n) {
-            if (cfg->tile_n != 32 && cfg->tile_n != 64) return QUICK_ERR_INVALID_ARG;
+            if (cfg->tile_n != 16 && cfg->tile_n != 32 && cfg->tile_n != 64) return QUICK_ERR_INVALID_ARG;
             pl->wn = cfg->tile_n;
         }
         if (cfg->split_k) {
@@ -712,11 +828,17 @@ void launch_stream_t(const uint16_t* x, const u4_t* pw, const uint16_t* ps, cons
 {
     const int NT = N / 16;
     dim3 grid((NT + NPW - 1) / NPW);
-    // Ring depth: more k-groups in flight where the activation fragments
-    // leave registers for it.
-    constexpr int D = MT == 1 ? 4 : 2;
-    hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D>), grid, dim3(64 * WAVES), 0, st, x, pw, ps,
-                       pz, y, M, N, K);
+    // activations staged in LDS when all of x fits (one padded slice per wave)
+    const size_t xbytes = (size_t)WAVES * stream_slice_bytes(M, K / 128, WAVES);
+    if (MT == 1 && xbytes <= kStreamLdsX) {
+        constexpr int D = NPW == 1 ? 16 : 8;
+        hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D, true>), grid, dim3(64 * WAVES), xbytes, st,
+                           x, pw, ps, pz, y, M, N, K);
+    } else {
+        constexpr int D = MT == 1 ? (NPW == 1 ? 8 : 4) : 2;
+        hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D, false>), grid, dim3(64 * WAVES), 0, st, x, pw, ps,
+                           pz, y, M, N, K);
+    }
 }
 
 template <int MT, int NPW>
@@ -770,7 +892,11 @@ void launch_tiled_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uin
 int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
                  const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st)
 {
-    if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
+    if (pl.bm == 16 && pl.wn == 32) launch_tiled_t<16, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
+    else if (pl.bm == 32 && pl.wn == 32) launch_tiled_t<32, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
+    else if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
+    else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
+    else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
     else if (pl.bm == 128 && pl.wn == 32) launch_tiled_t<128, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
     else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
     else return QUICK_ERR_INVALID_ARG;

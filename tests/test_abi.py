@@ -98,6 +98,7 @@ def test_gemm_ex_validation_without_device():
     assert ex(Q.make_config(variant=1, split_k=3)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=1, tile_n=3)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=2, tile_m=96)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=2, tile_m=16, tile_n=64)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=2, tile_n=48)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=2, split_k=33)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=2, tile_m=256, tile_n=64)) == Q.QUICK_ERR_INVALID_ARG

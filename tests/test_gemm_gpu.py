@@ -21,7 +21,8 @@ pytestmark = pytest.mark.gpu
 
 STREAM_CFGS = [dict(variant=1, split_k=w, tile_n=p) for w in (1, 2, 4, 8) for p in (1, 2)]
 TILED_CFGS = [dict(variant=2, tile_m=bm, tile_n=wn, split_k=s)
-              for bm, wn in ((64, 32), (64, 64), (128, 32)) for s in (1, 3)]
+              for bm, wn in ((16, 16), (16, 32), (32, 16), (32, 32), (64, 32), (64, 64), (128, 32))
+              for s in (1, 3)]
 
 
 def _check(M, K, N, cfg, seed):
