@@ -111,8 +111,10 @@ typedef struct quick_config {
     int variant;   /* 0 auto, 1 = stream kernel (small M), 2 = tiled kernel   */
     int split_k;   /* number of K slices (tiled kernel: across workgroups;
                       stream kernel: waves per workgroup), 0 = auto          */
-    int tile_m;    /* tiled kernel rows per workgroup: 64, 128 or 256         */
-    int tile_n;    /* tiled kernel columns per wave: 32 or 64
+    int tile_m;    /* tiled kernel rows per workgroup: 16, 32, 64 or 128;
+                      supported (tile_m, tile_n) pairs: (16|32, 16|32),
+                      (64, 32), (64, 64), (128, 32)                         */
+    int tile_n;    /* tiled kernel columns per wave: 16, 32 or 64
                       stream kernel: n-tiles per wave: 1 or 2                 */
 } quick_config_t;
 
