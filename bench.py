@@ -27,6 +27,10 @@ import numpy as np
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E, GB/s
 MFMA_F16_PEAK_TFLOPS = 2500.0  # MI355X dense fp16 matrix peak, TFLOP/s
 METRIC = "W4A16 GEMM TFLOPS + HBM GB/s vs roofline, M=1..1024, Llama-7B/70B shapes"
+ROOT = os.path.dirname(os.path.abspath(__file__))
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2402_10076_amd", "csrc", "quick_gemm.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_bench_llama2_7b_70b.json")
+COPY_CAL_BYTES = 256 << 20   # plain device copy used to scale the HBM byte counters
 
 
 def log(*a):
@@ -37,9 +41,106 @@ def kernel_name(sel: dict) -> str:
     if sel["variant"] == 1:
         return "stream_kernel<MT,%d,%d>" % (sel["tile_n"], sel["split_k"])
     name = "tiled_kernel<%d,%d>" % (sel["tile_m"], sel["tile_n"])
-    if sel["split_k"] > 1:
+    if sel["variant"] == 3:
+        name += "+streamK(G=%d)" % sel["split_k"]
+    elif sel["split_k"] > 1:
         name += "+splitk_reduce(S=%d)" % sel["split_k"]
     return name
+
+
+def kernel_source_digest() -> str:
+    """Identifies the kernel code a stored counter measurement belongs to."""
+    import hashlib
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def launch_sequence(points):
+    """Kernel launches of one step, in order: (bench kernel name, symbol prefix)."""
+    seq = []
+    for p in points:
+        sel = p["sel"]
+        if sel["variant"] == 1:
+            seq.append((p["kernel"], "stream_kernel<"))
+        else:
+            seq.append((p["kernel"], "tiled_kernel<%d, %d>" % (sel["tile_m"], sel["tile_n"])))
+            if sel["variant"] == 2 and sel["split_k"] > 1:
+                seq.append((None, "splitk_reduce_kernel"))
+    return seq
+
+
+def read_counter_csv(path: str, counter: str):
+    """[(dispatch id, kernel symbol, value)] of one rocprofv3 counter CSV, in dispatch order."""
+    import csv
+    rows = []
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] == counter:
+            rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"], float(r["Counter_Value"])))
+    rows.sort()
+    return rows
+
+
+def ingest_pmc(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, points, dominant):
+    """HBM bytes per launch of the dominant kernel from FETCH_SIZE / WRITE_SIZE
+    runs of one bench step, each scaled by what the counter reads for a plain
+    device-to-device copy of COPY_CAL_BYTES."""
+    seq = launch_sequence(points)
+    per = {}
+    for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
+        ours = [r for r in read_counter_csv(path, name)
+                if "anonymous namespace)::" in r[1] and "at::" not in r[1]]
+        if len(ours) != len(seq):
+            raise SystemExit("%s: %d library dispatches, expected %d" % (path, len(ours), len(seq)))
+        for (bname, prefix), r in zip(seq, ours):
+            if prefix not in r[1]:
+                raise SystemExit("dispatch %d is %s, expected %s" % (r[0], r[1][:80], prefix))
+        vals = [r[2] for (bname, _), r in zip(seq, ours) if bname == dominant]
+        per[name] = float(np.mean(vals))
+    cal = {}
+    for name, path in (("FETCH_SIZE", cal_fetch_csv), ("WRITE_SIZE", cal_write_csv)):
+        # the device-to-device copies of the calibration run (HIP runtime copy kernel)
+        v = [r[2] for r in read_counter_csv(path, name) if "copyBuffer" in r[1]]
+        top = max(v)
+        cal[name] = (COPY_CAL_BYTES / 1024.0) / float(np.median([x for x in v if x >= 0.9 * top]))
+    fetch_b = per["FETCH_SIZE"] * cal["FETCH_SIZE"] * 1024.0
+    write_b = per["WRITE_SIZE"] * cal["WRITE_SIZE"] * 1024.0
+    return {
+        "kernel": dominant,
+        "kernel_source_sha256_16": kernel_source_digest(),
+        "launches": int(sum(1 for b, _ in seq if b == dominant)),
+        "fetch_kib_per_dispatch": round(per["FETCH_SIZE"], 1),
+        "write_kib_per_dispatch": round(per["WRITE_SIZE"], 1),
+        "fetch_scale": round(cal["FETCH_SIZE"], 4),
+        "write_scale": round(cal["WRITE_SIZE"], 4),
+        "hbm_bytes_per_launch": int(round(fetch_b + write_b)),
+        "alg_bytes_per_launch": int(round(np.mean([p["bytes"] for p in points if p["kernel"] == dominant]))),
+    }
+
+
+def stored_traffic(dominant: str):
+    """HBM bytes per launch from the stored counter measurement, or None when
+    there is none for this kernel or the kernel source changed since."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel") != dominant or t.get("kernel_source_sha256_16") != kernel_source_digest():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def copy_calibration():
+    import torch
+    n = COPY_CAL_BYTES // 4
+    src = torch.arange(n, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    assert bool((dst == src).all())
+    log("copy calibration: 5 x %d MiB device copies" % (COPY_CAL_BYTES >> 20))
 
 
 def build_points(configs):
@@ -88,7 +189,28 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-col-fraction", type=float, default=1.0 / 32)
     ap.add_argument("--points-out", default="", help="optional path for the per-GEMM table (JSON)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a plain %d MiB device copy (scales rocprofv3 byte counters)" % (COPY_CAL_BYTES >> 20))
+    ap.add_argument("--ingest-pmc", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
+                    help="turn rocprofv3 FETCH_SIZE / WRITE_SIZE runs of one step (--steps 1 --warmup 0) and "
+                         "of --copy-calibration into the stored HBM traffic of the dominant kernel")
+    ap.add_argument("--dominant", default="tiled_kernel<128,32>", help="kernel name for --ingest-pmc")
     args = ap.parse_args()
+
+    if args.ingest_pmc:
+        import paper_2402_10076_amd as Q
+        points = build_points([int(c) for c in args.configs.split(",") if c])
+        import workloads as W
+        for p in points:
+            p["sel"] = Q.select_config(p["M"], p["N"], p["K"])
+            p["kernel"] = kernel_name(p["sel"])
+            p["bytes"] = W.alg_bytes(p["M"], p["N"], p["K"])
+        t = ingest_pmc(*args.ingest_pmc, points, args.dominant)
+        os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+        with open(TRAFFIC_FILE, "w") as f:
+            json.dump(t, f, indent=1)
+        print(json.dumps(t))
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -103,6 +225,9 @@ def main():
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     Q.lib()  # raises if the HIP library is not built
 
     configs = [int(c) for c in args.configs.split(",") if c]
@@ -197,9 +322,12 @@ def main():
         ach = sum(p["bytes"] for p in dpts) / (d_ms * 1e-3) / 1e9
         roof = dict(bound="hbm", achieved=round(ach, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(ach / HBM_PEAK_GBS, 4), traffic=None)
+    roof["traffic"] = stored_traffic(dom)
     roof["kernel"] = dom
     roof["launches_per_step"] = len(dpts)
     roof["avg_launch_us"] = round(d_ms * 1e3 / len(dpts), 2)
+    roof["alg_bytes_per_launch"] = int(round(np.mean([p["bytes"] for p in dpts])))
+    roof["alg_flops_per_launch"] = int(round(np.mean([p["flops"] for p in dpts])))
 
     small = [p for p in points if p["M"] <= 16]
     s_ms = sum(p["ms"] for p in small)

@@ -96,7 +96,8 @@ int quick_unpack_weights(const void* packed, const void* scales, const void* zer
  *   stream         hipStream_t passed as void*, NULL = default stream
  * M == 0 is a valid no-op.  The call returns after enqueueing; results are
  * visible after the stream is synchronized.  The library may use an internal
- * device workspace (split-K partial sums), allocated on first need per
+ * device workspace (split-K partial sums, stream-K partial tiles and arrival
+ * counters), allocated (counters zeroed) on first need per
  * (device, stream) and kept until process exit; a call that grows it
  * synchronizes `stream` first.  Calls on one stream are ordered; calls on
  * different streams use different workspaces.
@@ -108,9 +109,13 @@ int quick_w4a16_gemm(const void* x, const void* packed, const void* scales,
 /* Kernel selection for quick_w4a16_gemm_ex (tests, benchmarks, tuning).
  * Zero in any field means "choose automatically". */
 typedef struct quick_config {
-    int variant;   /* 0 auto, 1 = stream kernel (small M), 2 = tiled kernel   */
-    int split_k;   /* number of K slices (tiled kernel: across workgroups;
-                      stream kernel: waves per workgroup), 0 = auto          */
+    int variant;   /* 0 auto, 1 = stream kernel (small M), 2 = tiled kernel,
+                      3 = tiled kernel with the stream-K schedule (resident
+                      workgroups share the tiles x k-groups work equally)     */
+    int split_k;   /* variant 2: K slices across workgroups; variant 1: waves
+                      per workgroup (1, 2, 4, 8); variant 3: resident
+                      workgroups, a multiple of 8 up to 4096 (clamped to the
+                      number of tile x 128-channel units); 0 = auto          */
     int tile_m;    /* tiled kernel rows per workgroup: 16, 32, 64 or 128;
                       supported (tile_m, tile_n) pairs: (16|32, 16|32),
                       (64, 32), (64, 64), (128, 32)                         */
@@ -118,9 +123,16 @@ typedef struct quick_config {
                       stream kernel: n-tiles per wave: 1 or 2                 */
 } quick_config_t;
 
+/* Leading bytes of a workspace that hold stream-K arrival counters. */
+#define QUICK_WORKSPACE_COUNTER_BYTES 16384
+
 /* Same contract as quick_w4a16_gemm with an explicit kernel choice.
- * workspace/workspace_bytes: optional caller-owned device buffer for split-K
- * partial sums (16-byte aligned); when NULL the internal workspace is used.
+ * workspace/workspace_bytes: optional caller-owned device buffer (16-byte
+ * aligned) for split-K partial sums or stream-K partial tiles; when NULL the
+ * internal workspace is used.  Its first QUICK_WORKSPACE_COUNTER_BYTES hold
+ * arrival counters that must be zero before the buffer's first use (e.g.
+ * allocate it zero-filled); every call leaves them zero.  Calls that share a
+ * workspace must be ordered (same stream).
  * Errors as quick_w4a16_gemm, plus INVALID_ARG for an unsupported config
  * and WORKSPACE when the caller buffer is smaller than
  * quick_workspace_bytes(). */

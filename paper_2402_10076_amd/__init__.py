@@ -39,6 +39,10 @@ QUICK_ERR_WORKSPACE = 7
 VARIANT_AUTO = 0
 VARIANT_STREAM = 1
 VARIANT_TILED = 2
+VARIANT_STREAMK = 3
+
+# leading workspace bytes that hold stream-K arrival counters (QUICK_WORKSPACE_COUNTER_BYTES)
+WS_COUNTER_BYTES = 16384
 
 _lock = threading.Lock()
 _lib = None

@@ -407,13 +407,30 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 //
 // Tiles are numbered M-fastest and assigned so that consecutive numbers run
 // on the same XCD (workgroup ids go to the 8 XCDs round-robin): M-tiles that
-// share an N-tile's weights share one L2.  gridDim.x is padded to a multiple
-// of 8; the extra workgroups exit at once.  With splits > 1 each split writes
-// fp32 partial sums to the workspace and a second kernel adds them in split
-// order.
+// share an N-tile's weights share one L2.  Three schedules:
+//  * data-parallel (n_splits == 1): one workgroup per tile; gridDim.x is
+//    padded to a multiple of 8 and the extra workgroups exit at once;
+//  * split-K (n_splits > 1): one workgroup per (tile, K slice); each writes
+//    fp32 partial sums to the workspace and a second kernel adds them in
+//    split order;
+//  * stream-K (n_splits == 0): gridDim.x resident workgroups share the
+//    tiles x k-groups iteration space in equal contiguous ranges, so no
+//    round of tiles runs on a partly idle chip.  A tile whose k-groups span
+//    several workgroups is finished by the last of them to arrive (per-tile
+//    arrival counter): every contributor writes its fp32 partial tile with
+//    device-coherent stores, and the last one adds all partials in k order
+//    (the same order whoever is last, so results are deterministic), rounds
+//    once to f16 and resets the counter.  No workgroup ever waits for
+//    another.
 // ---------------------------------------------------------------------------
 constexpr int kTiledWaves = 8;
 constexpr int kTiledStages = 4;
+// stream-K workspace: arrival counters (one per workgroup, zero between
+// calls), then two fp32 partial-tile slots per workgroup
+constexpr int kSkMaxWorkgroups = 4096;
+constexpr size_t kSkCounterBytes = QUICK_WORKSPACE_COUNTER_BYTES;
+static_assert(kSkCounterBytes >= kSkMaxWorkgroups * sizeof(unsigned), "one counter per workgroup");
+constexpr int kCoherentAux = 0x11;  // sc0 sc1: coherent across XCDs, write-through
 
 template <int BM, int WN>
 __global__ void __launch_bounds__(64 * kTiledWaves, 1)
@@ -446,51 +463,45 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         return st == 0 ? lds_s0 : st == 1 ? lds_s1 : st == 2 ? lds_s2 : lds_s3;
     };
 
-    // ---- tile assignment (XCD-aware, M-fastest)
-    const int nblk = n_mtiles * n_ntiles * n_splits;
-    const int per_xcd = gridDim.x >> 3;
-    const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
-    if (t >= nblk) return;
-    const int mtile = t % n_mtiles;
-    const int ntile = (t / n_mtiles) % n_ntiles;
-    const int split = t / (n_mtiles * n_ntiles);
-
     const int KG = K >> 7;
     const int NT = N >> 4;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int c = lane & 15;
     const int g = lane >> 4;
-    const int m0 = mtile * BM;
-    const int kb = split * kg_per_split;
-    const int ke = min(KG, kb + kg_per_split);
 
     const rsrc_t rw = make_rsrc(pw, (uint32_t)((size_t)K * N / 2));
     const rsrc_t rs = make_rsrc(ps, (uint32_t)((size_t)K * N / 64));
     const rsrc_t rz = make_rsrc(pz, (uint32_t)((size_t)K * N / 256));
     const rsrc_t rx = make_rsrc(x, (uint32_t)((size_t)M * K * 2));
-
-    // weight units of this wave's n-tiles (clamped; out-of-range tiles are
-    // computed on valid data and never stored)
-    const int ntw = ntile * (WAVES * NP) + wave * NP;
-    uint32_t ubase[NP];
-#pragma unroll
-    for (int p = 0; p < NP; ++p) ubase[p] = (uint32_t)min(ntw + p, NT - 1) * KG;
     const uint32_t vw = lane * 16;
     const uint32_t vs = c * 2;
     const uint32_t vz = (c >> 3) * 4;
-
-    // LDS-DMA source offsets: this lane fills row rr of 1 KiB block i at chunk
-    // position (lane % 16), i.e. it fetches channel chunk (lane % 16) ^ (rr % 16).
     // this wave's DMA instruction count (wave-uniform)
     const int ndma = NDMA >= WAVES ? DMA_PER_WAVE : (wave < NDMA ? 1 : 0);
+
+    // ---- per-tile state
+    int m0 = 0;      // first row of the tile
+    int ntw = 0;     // first n-tile of this wave
+    uint32_t ubase[NP];
     uint32_t vx[DMA_PER_WAVE];
+    auto set_tile = [&](int mtile, int ntile) {
+        m0 = mtile * BM;
+        // weight units of this wave's n-tiles (clamped; out-of-range tiles
+        // are computed on valid data and never stored)
+        ntw = ntile * (WAVES * NP) + wave * NP;
 #pragma unroll
-    for (int i = 0; i < DMA_PER_WAVE; ++i) {
-        const int rr = (wave + i * WAVES) * 4 + (lane >> 4);
-        const int row = min(m0 + rr, M - 1);
-        vx[i] = (uint32_t)(row * K + 8 * ((lane & 15) ^ (rr & 15))) * 2;
-    }
+        for (int p = 0; p < NP; ++p) ubase[p] = (uint32_t)min(ntw + p, NT - 1) * KG;
+        // LDS-DMA source offsets: this lane fills row rr of 1 KiB block i at
+        // chunk position (lane % 16), i.e. it fetches channel chunk
+        // (lane % 16) ^ (rr % 16)
+#pragma unroll
+        for (int i = 0; i < DMA_PER_WAVE; ++i) {
+            const int rr = (wave + i * WAVES) * 4 + (lane >> 4);
+            const int row = min(m0 + rr, M - 1);
+            vx[i] = (uint32_t)(row * K + 8 * ((lane & 15) ^ (rr & 15))) * 2;
+        }
+    };
 
     u4_t wr[NST][NP];
     uint32_t sr[NST][NP], zr[NST][NP];
@@ -527,10 +538,6 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     };
 
     f4_t acc[NP][MTT];
-#pragma unroll
-    for (int p = 0; p < NP; ++p)
-#pragma unroll
-        for (int mt = 0; mt < MTT; ++mt) acc[p][mt] = f4_t{0.f, 0.f, 0.f, 0.f};
 
     // fragment read inside a stage: row mt*16 + c, chunk (4j+g) ^ c
     auto bfrag = [&](int st, int mt, int j) -> h8_t {
@@ -571,41 +578,48 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         }
     };
 
-    // prologue: k-groups kb .. kb+NST-2 in flight, then wait for kb
+    // acc = x[m0 .. m0+BM) [k-groups kb .. ke) . W[.., this wave's columns)
+    auto run = [&](int kb, int ke) {
 #pragma unroll
-    for (int i = 0; i < NST - 1; ++i)
-        if (kb + i < ke) fetch(i, kb + i);
-    wait_groups(min(NST - 2, ke - kb - 1));
-    barrier();
+        for (int p = 0; p < NP; ++p)
+#pragma unroll
+            for (int mt = 0; mt < MTT; ++mt) acc[p][mt] = f4_t{0.f, 0.f, 0.f, 0.f};
+        // prologue: k-groups kb .. kb+NST-2 in flight, then wait for kb
+#pragma unroll
+        for (int i = 0; i < NST - 1; ++i)
+            if (kb + i < ke) fetch(i, kb + i);
+        wait_groups(min(NST - 2, ke - kb - 1));
+        barrier();
 
-    // steady state: straight-line body (unconditional requests) so the
-    // compiler's own wait analysis keeps the requested k-groups in flight
-    int kg = kb;
-    for (; kg + 2 * NST - 1 <= ke; kg += NST) {
+        // steady state: straight-line body (unconditional requests) so the
+        // compiler's own wait analysis keeps the requested k-groups in flight
+        int kg = kb;
+        for (; kg + 2 * NST - 1 <= ke; kg += NST) {
 #pragma unroll
-        for (int i = 0; i < NST; ++i) {
-            fetch((i + NST - 1) % NST, kg + i + NST - 1);
-            kgroup(i);
-            // k-group kg+i+1 must have landed; later ones stay in flight
-            wait_groups(NST - 2);
-            barrier();
-        }
-    }
-    // tail
-    for (; kg < ke; kg += NST) {
-#pragma unroll
-        for (int i = 0; i < NST; ++i) {
-            const int k = kg + i;
-            if (k < ke) {
-                if (k + NST - 1 < ke) fetch((i + NST - 1) % NST, k + NST - 1);
+            for (int i = 0; i < NST; ++i) {
+                fetch((i + NST - 1) % NST, kg + i + NST - 1);
                 kgroup(i);
-                wait_groups(min(NST - 2, ke - k - 2));
+                // k-group kg+i+1 must have landed; later ones stay in flight
+                wait_groups(NST - 2);
                 barrier();
             }
         }
-    }
+        // tail
+        for (; kg < ke; kg += NST) {
+#pragma unroll
+            for (int i = 0; i < NST; ++i) {
+                const int k = kg + i;
+                if (k < ke) {
+                    if (k + NST - 1 < ke) fetch((i + NST - 1) % NST, k + NST - 1);
+                    kgroup(i);
+                    wait_groups(min(NST - 2, ke - k - 2));
+                    barrier();
+                }
+            }
+        }
+    };
 
-    if (n_splits == 1) {
+    auto store_y = [&](const f4_t (&v)[NP][MTT]) {
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
             if (ntw + p >= NT) continue;
@@ -613,11 +627,26 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 #pragma unroll
             for (int mt = 0; mt < MTT; ++mt) {
                 const int m = m0 + mt * 16 + c;
-                if (m < M) store_h4(y + (size_t)m * N + n, acc[p][mt]);
+                if (m < M) store_h4(y + (size_t)m * N + n, v[p][mt]);
             }
         }
-    } else {
-        float* part = ws + (size_t)split * M * N;
+    };
+
+    if (n_splits > 0) {
+        // ---- data-parallel / split-K: one (tile, K slice) per workgroup
+        const int nblk = n_mtiles * n_ntiles * n_splits;
+        const int per_xcd = gridDim.x >> 3;
+        const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+        if (t >= nblk) return;
+        const int split = t / (n_mtiles * n_ntiles);
+        set_tile(t % n_mtiles, (t / n_mtiles) % n_ntiles);
+        const int kb = split * kg_per_split;
+        run(kb, min(KG, kb + kg_per_split));
+        if (n_splits == 1) {
+            store_y(acc);
+            return;
+        }
+        float* part = ws + kSkCounterBytes / sizeof(float) + (size_t)split * M * N;
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
             if (ntw + p >= NT) continue;
@@ -628,6 +657,80 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
                 if (m < M) *reinterpret_cast<f4_t*>(part + (size_t)m * N + n) = acc[p][mt];
             }
         }
+        return;
+    }
+
+    // ---- stream-K: this workgroup owns units [u0, u1) of tiles x k-groups
+    // (the host launches 8 <= gridDim.x <= tiles * KG, a multiple of 8, so
+    // every range is non-empty and a tile's contributors are consecutive)
+    const int G = gridDim.x;
+    const int wid = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+    const int64_t U = (int64_t)n_mtiles * n_ntiles * KG;
+    const int64_t u0 = (int64_t)wid * U / G;
+    const int64_t u1 = (int64_t)(wid + 1) * U / G;
+    unsigned* counters = reinterpret_cast<unsigned*>(ws);
+    // partial-tile slot: thread-major f4 at ((wave * NP + p) * MTT + mt) * 64 + lane
+    constexpr uint32_t SLOT_BYTES = (uint32_t)WAVES * NP * MTT * 64 * 16;
+    const rsrc_t rp = make_rsrc(ws + kSkCounterBytes / sizeof(float), (uint32_t)(2 * G) * SLOT_BYTES);
+    auto slot_off = [&](int p, int mt) -> uint32_t {
+        return (uint32_t)((((wave * NP + p) * MTT + mt) * 64 + lane) * 16);
+    };
+    __shared__ int sk_last;
+    for (int64_t u = u0; u < u1;) {
+        const int tt = (int)(u / KG);
+        const int kb = (int)(u - (int64_t)tt * KG);
+        const int ke = (int)min<int64_t>(KG, kb + (u1 - u));
+        set_tile(tt % n_mtiles, tt / n_mtiles);
+        run(kb, ke);
+        if (kb == 0 && ke == KG) {
+            store_y(acc);
+        } else {
+            const int64_t tb = (int64_t)tt * KG;
+            const int w0 = (int)(((tb + 1) * G - 1) / U);        // owner of the tile's first unit
+            const int w1 = (int)(((tb + KG) * G - 1) / U);       // ... and of its last
+            // slot 2w: the piece that starts w's range; 2w+1: the piece that ends it
+            const uint32_t mine = uniform((uint32_t)(2 * wid + (u == u0 ? 0 : 1)) * SLOT_BYTES);
+#pragma unroll
+            for (int p = 0; p < NP; ++p)
+#pragma unroll
+                for (int mt = 0; mt < MTT; ++mt)
+                    __builtin_amdgcn_raw_buffer_store_b128(bits_as<u4_t>(acc[p][mt]), rp, slot_off(p, mt), mine,
+                                                           kCoherentAux);
+            wait_all();       // this wave's partial is written through
+            __syncthreads();  // ... and every wave's
+            if (threadIdx.x == 0)
+                sk_last = __hip_atomic_fetch_add(&counters[w1], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                          (unsigned)(w1 - w0);
+            __syncthreads();
+            if (sk_last) {
+                // sum the pieces in k order: contributor w0, w0+1, .., w1
+#pragma unroll
+                for (int p = 0; p < NP; ++p) {
+#pragma unroll
+                    for (int mt = 0; mt < MTT; ++mt) {
+                        f4_t sum = f4_t{0.f, 0.f, 0.f, 0.f};
+                        for (int w = w0; w <= w1; ++w) {
+                            f4_t v;
+                            if (w == wid) {
+                                v = acc[p][mt];
+                            } else {
+                                const int first = (int64_t)w * U / G >= tb ? 0 : 1;
+                                v = bits_as<f4_t>(__builtin_amdgcn_raw_buffer_load_b128(
+                                    rp, slot_off(p, mt), uniform((uint32_t)(2 * w + first) * SLOT_BYTES),
+                                    kCoherentAux));
+                            }
+                            sum = w == w0 ? v : sum + v;
+                        }
+                        acc[p][mt] = sum;
+                    }
+                }
+                store_y(acc);
+                if (threadIdx.x == 0)
+                    __hip_atomic_store(&counters[w1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        u += ke - kb;
+        __syncthreads();  // LDS stages and sk_last are reused by the next piece
     }
 }
 
@@ -650,16 +753,63 @@ splitk_reduce_kernel(const float* __restrict__ ws, uint16_t* __restrict__ y, int
 constexpr int kVariantStream = 1;
 constexpr size_t kStreamLdsX = 64 * 1024;  // LDS bytes the stream kernel may give to activations
 constexpr int kVariantTiled = 2;
+constexpr int kVariantStreamK = 3;  // tiled kernel, stream-K schedule
 
 struct Plan {
     int variant;
-    int split;  // stream: waves per workgroup; tiled: k splits
+    int split;  // stream: waves per workgroup; tiled: k splits; stream-K: workgroups
     int bm;     // tiled: rows per workgroup
     int wn;     // tiled: columns per wave; stream: n-tiles per wave
     int kgps;   // tiled: k-groups per split
 };
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+bool is_tiled(int variant) { return variant == kVariantTiled || variant == kVariantStreamK; }
+
+// Bytes of one stream-K partial-tile slot.
+size_t sk_slot_bytes(int bm, int wn) { return (size_t)bm * kTiledWaves * wn * sizeof(float); }
+
+template <int BM, int WN>
+int tiled_resident_per_cu()
+{
+    int n = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(&tiled_kernel<BM, WN>),
+                                                     64 * kTiledWaves, 0) != hipSuccess || n < 1)
+        n = 1;
+    return n;
+}
+
+// Workgroups of the tiled kernel that are resident at once on the current
+// device (compute units x workgroups per compute unit); 256 when no device
+// can be queried.
+int tiled_resident(int bm, int wn)
+{
+    static std::mutex mu;
+    static std::map<std::pair<int, int>, int> cache;  // (device, tile id) -> workgroups
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) {
+        (void)hipGetLastError();
+        return 256;
+    }
+    const int id = bm * 1000 + wn;
+    std::lock_guard<std::mutex> lk(mu);
+    auto it = cache.find({dev, id});
+    if (it != cache.end()) return it->second;
+    int per = 1;
+    if (bm == 16 && wn == 16) per = tiled_resident_per_cu<16, 16>();
+    else if (bm == 16 && wn == 32) per = tiled_resident_per_cu<16, 32>();
+    else if (bm == 32 && wn == 16) per = tiled_resident_per_cu<32, 16>();
+    else if (bm == 32 && wn == 32) per = tiled_resident_per_cu<32, 32>();
+    else if (bm == 64 && wn == 32) per = tiled_resident_per_cu<64, 32>();
+    else if (bm == 64 && wn == 64) per = tiled_resident_per_cu<64, 64>();
+    else if (bm == 128 && wn == 32) per = tiled_resident_per_cu<128, 32>();
+    (void)hipGetLastError();
+    const int g = std::min(cus * per, kSkMaxWorkgroups);
+    cache[{dev, id}] = g;
+    return g;
+}
 
 int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
 {
@@ -708,11 +858,23 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
         stream_plan();
         return QUICK_OK;
     }
+    pl->kgps = 0;
+    // At least half as many tiles as resident workgroups, but not a whole
+    // number of rounds, and a long K: stream-K spreads the tiles x k-groups
+    // work evenly and each split tile has only a few pieces to add.  Short K
+    // (each piece's pipeline fill and partial-tile traffic weigh more) or
+    // fewer tiles: split-K, whose separate reduction pass spreads the adding
+    // over the whole chip.
+    const int64_t resident = tiled_resident(pl->bm, pl->wn);
+    if (pl->bm >= 64 && KG >= 48 && tiles % resident != 0 && 2 * tiles >= resident) {
+        pl->variant = kVariantStreamK;
+        pl->split = 0;
+        return QUICK_OK;
+    }
     const int64_t target = pl->wn == 16 ? 384 : 160;
     int s = 1;
     while (tiles * s < target && KG / (2 * s) >= 4 && s < 8) s *= 2;
     pl->split = s;
-    pl->kgps = 0;
     return QUICK_OK;
 }
 
@@ -727,7 +889,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
     auto_plan(M, N, K, pl);
     if (!cfg) return QUICK_OK;
     const int64_t KG = K / 128;
-    if (cfg->variant < 0 || cfg->variant > 2 || cfg->split_k < 0) return QUICK_ERR_INVALID_ARG;
+    if (cfg->variant < 0 || cfg->variant > 3 || cfg->split_k < 0) return QUICK_ERR_INVALID_ARG;
     if (cfg->variant == kVariantStream) {
         if (M > 64) return QUICK_ERR_INVALID_ARG;
         if (pl->variant != kVariantStream) auto_plan(std::min<int64_t>(M, 64), N, K, pl);
@@ -741,15 +903,22 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
             if (cfg->tile_n != 1 && cfg->tile_n != 2) return QUICK_ERR_INVALID_ARG;
             pl->wn = cfg->tile_n;
         }
-    } else if (cfg->variant == kVariantTiled) {
-        if (pl->variant != kVariantTiled) {
-            pl->variant = kVariantTiled;
+    } else if (cfg->variant == kVariantTiled || cfg->variant == kVariantStreamK) {
+        if (!is_tiled(pl->variant)) {
             pl->bm = 64;
             pl->wn = 32;
             pl->split = 1;
         }
+        if (pl->variant != cfg->variant) pl->split = cfg->variant == kVariantStreamK ? 0 : 1;
+        pl->variant = cfg->variant;
     }
-    if (pl->variant == kVariantTiled) {
+    if (pl->variant == kVariantStreamK) {
+        // split_k: persistent workgroups, a multiple of 8 (0 = all resident)
+        if (cfg->split_k && (cfg->split_k % 8 != 0 || cfg->split_k > kSkMaxWorkgroups))
+            return QUICK_ERR_INVALID_ARG;
+        pl->split = cfg->split_k;
+    }
+    if (is_tiled(pl->variant)) {
         if (cfg->tile_m) {
             if (cfg->tile_m != 16 && cfg->tile_m != 32 && cfg->tile_m != 64 && cfg->tile_m != 128)
                 return QUICK_ERR_INVALID_ARG;
@@ -759,7 +928,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
             if (cfg->tile_n != 16 && cfg->tile_n != 32 && cfg->tile_n != 64) return QUICK_ERR_INVALID_ARG;
             pl->wn = cfg->tile_n;
         }
-        if (cfg->split_k) {
+        if (cfg->split_k && pl->variant == kVariantTiled) {
             if (cfg->split_k > KG) return QUICK_ERR_INVALID_ARG;
             pl->split = cfg->split_k;
         }
@@ -768,8 +937,22 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
     return QUICK_OK;
 }
 
-void finish_plan(int64_t K, Plan* pl)
+void finish_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
 {
+    if (pl->variant == kVariantStreamK) {
+        // 8 <= workgroups <= tiles x k-groups, a multiple of 8: every
+        // workgroup gets a non-empty range and the XCD mapping is exact
+        const int64_t units = (int64_t)ceil_div(M, pl->bm) * ceil_div(N, kTiledWaves * pl->wn) * (K / 128);
+        int64_t g = pl->split ? pl->split : tiled_resident(pl->bm, pl->wn);
+        g = std::min<int64_t>(g, units) / 8 * 8;
+        if (g >= 8) {
+            pl->split = (int)g;
+            pl->kgps = 0;
+            return;
+        }
+        pl->variant = kVariantTiled;  // too little work: one workgroup per tile
+        pl->split = 1;
+    }
     if (pl->variant == kVariantTiled) {
         const int64_t KG = K / 128;
         if (pl->split > KG) pl->split = (int)KG;
@@ -779,9 +962,13 @@ void finish_plan(int64_t K, Plan* pl)
     }
 }
 
+// Workspace layout: kSkCounterBytes of stream-K arrival counters (zero
+// between calls), then split-K partial outputs or stream-K partial tiles.
 size_t plan_workspace(int64_t M, int64_t N, const Plan& pl)
 {
-    if (pl.variant == kVariantTiled && pl.split > 1) return (size_t)pl.split * M * N * sizeof(float);
+    if (pl.variant == kVariantTiled && pl.split > 1)
+        return kSkCounterBytes + (size_t)pl.split * M * N * sizeof(float);
+    if (pl.variant == kVariantStreamK) return kSkCounterBytes + 2 * (size_t)pl.split * sk_slot_bytes(pl.bm, pl.wn);
     return 0;
 }
 
@@ -816,6 +1003,8 @@ int get_workspace(size_t need, hipStream_t stream, void** out)
             b.ptr = nullptr;
             return QUICK_ERR_HIP;
         }
+        // stream-K arrival counters start at zero (every call leaves them zero)
+        if (hipMemsetAsync(b.ptr, 0, kSkCounterBytes, stream) != hipSuccess) return QUICK_ERR_HIP;
         b.bytes = sz;
     }
     *out = b.ptr;
@@ -883,6 +1072,11 @@ void launch_tiled_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uin
 {
     const int nm = ceil_div(M, BM);
     const int nn = ceil_div(N, kTiledWaves * WN);
+    if (pl.variant == kVariantStreamK) {
+        hipLaunchKernelGGL((tiled_kernel<BM, WN>), dim3(pl.split), dim3(64 * kTiledWaves), 0, st, x, pw, ps, pz,
+                           y, ws, M, N, K, 0, nm, nn, 0);
+        return;
+    }
     const int nblk = nm * nn * pl.split;
     const int grid = ceil_div(nblk, 8) * 8;
     hipLaunchKernelGGL((tiled_kernel<BM, WN>), dim3(grid), dim3(64 * kTiledWaves), 0, st, x, pw, ps, pz, y,
@@ -900,11 +1094,11 @@ int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16
     else if (pl.bm == 128 && pl.wn == 32) launch_tiled_t<128, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
     else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
     else return QUICK_ERR_INVALID_ARG;
-    if (pl.split > 1) {
+    if (pl.variant == kVariantTiled && pl.split > 1) {
         const int64_t MN = (int64_t)M * N;
         const int64_t MN4 = MN / 4;
         hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((MN4 + 255) / 256)), dim3(256), 0, st,
-                           ws, y, MN4, MN, pl.split);
+                           ws + kSkCounterBytes / sizeof(float), y, MN4, MN, pl.split);
     }
     return QUICK_OK;
 }
@@ -942,7 +1136,7 @@ int gemm_impl(const void* x, const void* packed, const void* scales, const void*
     st = make_plan(M, N, K, cfg, &pl);
     if (st) return st;
     if (M == 0) return QUICK_OK;
-    finish_plan(K, &pl);
+    finish_plan(M, N, K, &pl);
     hipStream_t hs = (hipStream_t)stream;
     const size_t need = plan_workspace(M, N, pl);
     void* ws = nullptr;
@@ -994,7 +1188,7 @@ extern "C" size_t quick_workspace_bytes(int64_t M, int64_t N, int64_t K, const q
     if (M <= 0 || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return 0;
     Plan pl;
     if (make_plan(M, N, K, cfg, &pl)) return 0;
-    finish_plan(K, &pl);
+    finish_plan(M, N, K, &pl);
     return plan_workspace(M, N, pl);
 }
 
@@ -1004,10 +1198,10 @@ extern "C" int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config
     if (M < 0 || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return QUICK_ERR_SHAPE;
     Plan pl;
     auto_plan(M, N, K, &pl);
-    finish_plan(K, &pl);
+    finish_plan(M, N, K, &pl);
     cfg->variant = pl.variant;
     cfg->split_k = pl.split;
-    cfg->tile_m = pl.variant == kVariantTiled ? pl.bm : 0;
+    cfg->tile_m = is_tiled(pl.variant) ? pl.bm : 0;
     cfg->tile_n = pl.wn;
     return QUICK_OK;
 }

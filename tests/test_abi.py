@@ -93,7 +93,10 @@ def test_gemm_ex_validation_without_device():
     L = Q.lib()
     def ex(cfg, M=4, N=4096, K=4096, ws=None, wsb=0):
         return L.quick_w4a16_gemm_ex(A, A, A, A, A, M, N, K, 128, None, ctypes.byref(cfg), ws, wsb)
-    assert ex(Q.make_config(variant=3)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=4)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=3, split_k=12)) == Q.QUICK_ERR_INVALID_ARG   # not a multiple of 8
+    assert ex(Q.make_config(variant=3, split_k=8192)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=3, tile_m=128, tile_n=64)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=1), M=65) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=1, split_k=3)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=1, tile_n=3)) == Q.QUICK_ERR_INVALID_ARG
@@ -105,9 +108,17 @@ def test_gemm_ex_validation_without_device():
     assert ex(Q.make_config(variant=2, tile_m=128, tile_n=64)) == Q.QUICK_ERR_INVALID_ARG
     cfg = Q.make_config(variant=2, tile_m=128, tile_n=32, split_k=4)
     need = Q.workspace_bytes(256, 4096, 4096, cfg)
-    assert need == 4 * 256 * 4096 * 4
+    assert need == Q.WS_COUNTER_BYTES + 4 * 256 * 4096 * 4
     assert ex(cfg, M=256, ws=A, wsb=need - 1) == Q.QUICK_ERR_WORKSPACE
     assert ex(cfg, M=256, ws=A + 4, wsb=need) == Q.QUICK_ERR_ALIGNMENT
+    # stream-K: counters, then two fp32 partial tiles (128 x 256) per workgroup
+    sk = Q.make_config(variant=3, tile_m=128, tile_n=32, split_k=64)
+    assert Q.workspace_bytes(256, 4096, 4096, sk) == Q.WS_COUNTER_BYTES + 2 * 64 * 128 * 256 * 4
+    # more workgroups than (tile, k-group) units: clamped to the units (2 x 16 x 32 = 1024)
+    sk = Q.make_config(variant=3, tile_m=128, tile_n=32, split_k=4096)
+    assert Q.workspace_bytes(256, 4096, 4096, sk) == Q.WS_COUNTER_BYTES + 2 * 1024 * 128 * 256 * 4
+    # fewer than 8 units: one workgroup per tile, no workspace
+    assert Q.workspace_bytes(16, 128, 512, Q.make_config(variant=3, tile_m=16, tile_n=16)) == 0
 
 
 def test_select_config_regimes():

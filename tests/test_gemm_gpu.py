@@ -20,9 +20,11 @@ from gpu_util import TOL, Packed, f16_values, from_dev_y, rand_case, rel_err, ru
 pytestmark = pytest.mark.gpu
 
 STREAM_CFGS = [dict(variant=1, split_k=w, tile_n=p) for w in (1, 2, 4, 8) for p in (1, 2)]
-TILED_CFGS = [dict(variant=2, tile_m=bm, tile_n=wn, split_k=s)
-              for bm, wn in ((16, 16), (16, 32), (32, 16), (32, 32), (64, 32), (64, 64), (128, 32))
-              for s in (1, 3)]
+TILES = ((16, 16), (16, 32), (32, 16), (32, 32), (64, 32), (64, 64), (128, 32))
+TILED_CFGS = [dict(variant=2, tile_m=bm, tile_n=wn, split_k=s) for bm, wn in TILES for s in (1, 3)]
+# stream-K: 8 and 24 resident workgroups split most tiles across workgroups;
+# 0 = all resident workgroups (clamped to the work units)
+STREAMK_CFGS = [dict(variant=3, tile_m=bm, tile_n=wn, split_k=g) for bm, wn in TILES for g in (8, 24, 0)]
 
 
 def _check(M, K, N, cfg, seed):
@@ -47,6 +49,21 @@ def test_stream_variants(M, cfg):
 def test_tiled_variants(M, cfg):
     for K, N in ((384, 80), (640, 528)):
         _check(M, K, N, cfg, seed=M * 1000 + K + N + 7)
+
+
+@pytest.mark.parametrize("cfg", STREAMK_CFGS, ids=lambda c: "bm%d_wn%d_g%d" % (c["tile_m"], c["tile_n"], c["split_k"]))
+@pytest.mark.parametrize("M", [1, 65, 300])
+def test_streamk_variants(M, cfg):
+    for K, N in ((384, 80), (640, 528), (2304, 272)):
+        _check(M, K, N, cfg, seed=M * 1000 + K + N + 11)
+
+
+@pytest.mark.parametrize("G", [16, 32, 64])
+def test_streamk_many_pieces_per_tile(G):
+    """One output tile, 32 k-groups over G workgroups: every tile is summed
+    from G / 1 .. pieces by the last arriving workgroup."""
+    _check(16, 4096, 128, dict(variant=3, tile_m=16, tile_n=16, split_k=G), seed=G)
+    _check(100, 4096, 256, dict(variant=3, tile_m=128, tile_n=32, split_k=G), seed=G + 1)
 
 
 @pytest.mark.parametrize("M", [1, 2, 5, 16, 31, 64, 65, 96, 127, 200, 513])
@@ -82,7 +99,7 @@ def test_one_hot_rows_give_exact_dequant(cfg):
     assert np.array_equal(y, want), "dequantized value mismatch at %d entries" % int((y != want).sum())
 
 
-@pytest.mark.parametrize("cfg", [None] + STREAM_CFGS[::3] + TILED_CFGS[::3])
+@pytest.mark.parametrize("cfg", [None] + STREAM_CFGS[::3] + TILED_CFGS[::3] + STREAMK_CFGS[::4])
 def test_integer_data_exact_under_any_split(cfg):
     """s = 1, z = 8, q in {7,8,9}, x in {-1,0,1}: every partial sum is a small
     integer, so any summation order is exact and y equals int64 x . (q - z)."""
@@ -159,6 +176,32 @@ def test_caller_workspace_and_side_stream():
     small = torch.empty(need // 8, dtype=torch.float32, device="cuda")
     with pytest.raises(Q.QuickError):
         p.gemm(xd, cfg=cfg, workspace=small)
+
+
+def test_streamk_caller_workspace_reuse_and_determinism():
+    M, K, N = 300, 2304, 528
+    x, q, z, s = rand_case(41, M, K, N)
+    p = Packed(q, z, s)
+    xd = to_dev_x(x)
+    cfg = Q.make_config(variant=3, tile_m=64, tile_n=32, split_k=24)
+    need = Q.workspace_bytes(M, N, K, cfg)
+    assert need > Q.WS_COUNTER_BYTES
+    ws = torch.zeros(need // 4, dtype=torch.float32, device="cuda")  # counters start at zero
+    y0 = from_dev_y(p.gemm(xd, cfg=cfg, workspace=ws))
+    assert rel_err(y0, oracle.gemm(x, q, z, s)) <= TOL
+    torch.cuda.synchronize()
+    # every call leaves the counters at zero, and the fixed k-order sum makes
+    # repeated calls bit-identical
+    assert int(torch.count_nonzero(ws[:Q.WS_COUNTER_BYTES // 4])) == 0
+    for _ in range(3):
+        assert np.array_equal(from_dev_y(p.gemm(xd, cfg=cfg, workspace=ws)), y0)
+    assert int(torch.count_nonzero(ws[:Q.WS_COUNTER_BYTES // 4])) == 0
+    # the same through the library-owned workspace, interleaved with split-K
+    # calls that share it
+    sk2 = Q.make_config(variant=2, tile_m=64, tile_n=32, split_k=3)
+    for _ in range(2):
+        assert np.array_equal(from_dev_y(p.gemm(xd, cfg=cfg)), y0)
+        assert rel_err(from_dev_y(p.gemm(xd, cfg=sk2)), f16_values(y0)) <= TOL
 
 
 def test_m_zero_is_noop():
