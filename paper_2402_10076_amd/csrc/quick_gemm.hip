@@ -485,7 +485,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     int ntw = 0;     // first n-tile of this wave
     uint32_t ubase[NP];
     uint32_t vx[DMA_PER_WAVE];
-    auto set_tile = [&](int mtile, int ntile) {
+    auto set_tile = [&](int mtile, int ntile) __attribute__((always_inline)) {
         m0 = mtile * BM;
         // weight units of this wave's n-tiles (clamped; out-of-range tiles
         // are computed on valid data and never stored)
@@ -506,7 +506,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     u4_t wr[NST][NP];
     uint32_t sr[NST][NP], zr[NST][NP];
     // k-group kg's activations -> LDS stage st and weights -> ring slot st
-    auto fetch = [&](int st, int kg) {
+    auto fetch = [&](int st, int kg) __attribute__((always_inline)) {
         const uint32_t soff = uniform((uint32_t)kg * 256u);
 #pragma unroll
         for (int i = 0; i < DMA_PER_WAVE; ++i)
@@ -545,7 +545,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         return bits_as<h8_t>(*reinterpret_cast<const u4_t*>(src));
     };
 
-    auto kgroup = [&](int st) {
+    auto kgroup = [&](int st) __attribute__((always_inline)) {
         Deq d[NP];
 #pragma unroll
         for (int p = 0; p < NP; ++p) d[p] = make_deq(sr[st][p], (zr[st][p] >> (4 * (c & 7))) & 15u);
@@ -579,7 +579,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     };
 
     // acc = x[m0 .. m0+BM) [k-groups kb .. ke) . W[.., this wave's columns)
-    auto run = [&](int kb, int ke) {
+    auto run = [&](int kb, int ke) __attribute__((always_inline)) {
 #pragma unroll
         for (int p = 0; p < NP; ++p)
 #pragma unroll
@@ -619,7 +619,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         }
     };
 
-    auto store_y = [&](const f4_t (&v)[NP][MTT]) {
+    auto store_y = [&](const f4_t (&v)[NP][MTT]) __attribute__((always_inline)) {
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
             if (ntw + p >= NT) continue;
@@ -845,12 +845,21 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
         const bool wide = (int64_t)ceil_div(M, 64) * ceil_div(N, 256) >= 160;
         pl->bm = wide ? 64 : 32;
         pl->wn = wide ? 32 : 16;
-    } else if (M <= 96) {
-        pl->bm = 64;
-        pl->wn = 32;
     } else {
-        pl->bm = 128;
-        pl->wn = 32;
+        // The largest tile whose K slices stay long: a split that leaves few
+        // k-groups per workgroup pays the pipeline fill and the partial-sum
+        // pass for little work, and a smaller tile that needs less splitting
+        // wins (narrow N or short K).
+        static const int cand[3][2] = {{128, 32}, {64, 32}, {32, 16}};
+        for (int c = M <= 96 ? 1 : 0; c < 3; ++c) {
+            pl->bm = cand[c][0];
+            pl->wn = cand[c][1];
+            const int64_t t = (int64_t)ceil_div(M, pl->bm) * ceil_div(N, kTiledWaves * pl->wn);
+            const int64_t tgt = pl->wn == 16 ? 256 : 160;
+            int s = 1;
+            while (t * s < tgt && KG / (2 * s) >= 4 && s < 8) s *= 2;
+            if (ceil_div(KG, s) >= 12) break;
+        }
     }
     const int64_t tiles = (int64_t)ceil_div(M, pl->bm) * ceil_div(N, kTiledWaves * pl->wn);
     if (pl->bm == 16 && tiles < 48) {
@@ -871,7 +880,7 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
         pl->split = 0;
         return QUICK_OK;
     }
-    const int64_t target = pl->wn == 16 ? 384 : 160;
+    const int64_t target = pl->wn == 16 ? (M > 64 ? 256 : 384) : 160;
     int s = 1;
     while (tiles * s < target && KG / (2 * s) >= 4 && s < 8) s *= 2;
     pl->split = s;
