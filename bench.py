@@ -129,6 +129,70 @@ def ingest_pmc(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, points, domin
     }
 
 
+def ingest_trace(trace_csv, points, dominant, out_md, command):
+    """Kernel durations per GEMM of the step from a rocprofv3 kernel trace of
+    a bench run (the run issues the step's launch sequence a whole number of
+    times), written as a markdown table; returns the dominant kernel's mean
+    duration in microseconds."""
+    import csv
+    seq = launch_sequence(points)
+    rows = []
+    for r in csv.DictReader(open(trace_csv)):
+        if "anonymous namespace)::" in r["Kernel_Name"] and "at::" not in r["Kernel_Name"]:
+            rows.append((int(r["Dispatch_Id"]), r["Kernel_Name"],
+                         (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-3))
+    rows.sort()
+    # whole repetitions of the step from the start (eager warm-up, graph
+    # replays, eager event steps); the subset-graph replays that follow are
+    # not used
+    reps = 0
+    while (reps + 1) * len(seq) <= len(rows) and all(
+            prefix in rows[reps * len(seq) + i][1] for i, (_, prefix) in enumerate(seq)):
+        reps += 1
+    if reps == 0:
+        raise SystemExit("%s: the library dispatches do not start with the step's launch sequence" % trace_csv)
+    # per point: its kernels' durations (tiled kernel + reduction when split), per repetition
+    per_point = [[0.0] * reps for _ in points]
+    dom_launch = []
+    j = 0
+    for rep in range(reps):
+        for i, p in enumerate(points):
+            n = 2 if (p["sel"]["variant"] == 2 and p["sel"]["split_k"] > 1) else 1
+            for t in range(n):
+                per_point[i][rep] += rows[j + t][2]
+            if p["kernel"] == dominant:
+                dom_launch.append(rows[j][2])
+            j += n
+    lines = ["| cfg | shape | K | N | M | kernel | mean us | min us | GB/s | TFLOP/s |",
+             "|---|---|---|---|---|---|---|---|---|---|"]
+    tot = 0.0
+    for i, p in enumerate(points):
+        mu = float(np.mean(per_point[i]))
+        tot += mu
+        lines.append("| C%d | %s | %d | %d | %d | %s | %.2f | %.2f | %.0f | %.1f |" % (
+            p["cid"], p["shape"], p["K"], p["N"], p["M"], p["kernel"], mu, min(per_point[i]),
+            p["bytes"] / mu / 1e3, p["flops"] / mu / 1e6))
+    dom_us = float(np.mean(dom_launch))
+    small = [i for i, p in enumerate(points) if p["M"] <= 16]
+    s_us = sum(float(np.mean(per_point[i])) for i in small)
+    s_gbs = sum(points[i]["bytes"] for i in small) / s_us / 1e3
+    with open(out_md, "w") as f:
+        f.write("# Kernel durations of the bench step (rocprofv3 kernel trace)\n\n")
+        f.write("Command (from the repository root on the GPU box, after `cd /tmp && export TMPDIR=/tmp`):\n\n")
+        f.write("```\n%s\n```\n\n" % command)
+        f.write("Then `python bench.py --ingest-trace <kernel_trace.csv> --trace-out <this file>` (CPU).\n\n")
+        f.write("%d library dispatches = %d repetitions of the step's %d launches (eager warm-up, "
+                "graph replays, eager event steps); each row averages the point's kernel time "
+                "(tiled kernel + split-K reduction where split) over the repetitions.\n\n" % (
+                    len(rows), reps, len(seq)))
+        f.write("* Dominant kernel `%s`: %d launches per step, mean kernel duration **%.2f us**.\n" % (
+            dominant, sum(1 for p in points if p["kernel"] == dominant), dom_us))
+        f.write("* Sum of kernel time per step: %.1f us.\n" % tot)
+        f.write("* GEMMs with M <= 16: %.1f us of kernels, %.0f GB/s of algorithmic bytes.\n\n" % (s_us, s_gbs))
+        f.write("\n".join(lines) + "\n")
+    return dom_us
+
+
 def stored_traffic(dominant: str):
     """HBM bytes per launch from the stored counter measurement, or None when
     there is none for this kernel or the kernel source changed since."""
@@ -153,6 +217,51 @@ def copy_calibration():
     torch.cuda.synchronize()
     assert bool((dst == src).all())
     log("copy calibration: 5 x %d MiB device copies" % (COPY_CAL_BYTES >> 20))
+
+
+def compare_fp16(K, N, Ms, reps=20):
+    """Context only: the W4A16 GEMM beside an fp16 GEMM of the same shape
+    through torch (hipBLASLt) on the dequantized weights, each timed with HIP
+    events over `reps` back-to-back launches that rotate through enough
+    weight copies to stream from HBM."""
+    import torch
+    import paper_2402_10076_amd as Q
+    import workloads as W
+    q, z, s = W.draw_weights(5, 1, K, N)
+    pw, ps, pz = Q.pack_weights(q, z, s)
+    wq = Q.to_device(pw, ps, pz)
+    # fp16 weights for the reference GEMM, dequantized on the device by the
+    # library itself (one-hot activations select the rows of W)
+    eye = torch.eye(K, dtype=torch.float16, device="cuda")
+    w16 = Q.w4a16_gemm(eye, *wq, N)
+    del eye
+    wbytes = K * N // 2
+    nq = max(2, -(-(1 << 30) // wbytes))
+    n16 = max(2, -(-(1 << 30) // (2 * K * N)))
+    qcopies = [tuple(t.clone() for t in wq) for _ in range(nq)]
+    hcopies = [w16.clone() for _ in range(n16)]
+    rows = []
+    for M in Ms:
+        x = torch.randn(M, K, device="cuda").half()
+        y = torch.empty(M, N, device="cuda", dtype=torch.float16)
+
+        def timed(fn):
+            for i in range(3):
+                fn(i)
+            torch.cuda.synchronize()
+            torch.cuda._sleep(5_000_000)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(reps):
+                fn(i)
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / reps * 1e3
+        t_q = timed(lambda i: Q.w4a16_gemm(x, *qcopies[i % nq], N, y=y))
+        t_h = timed(lambda i: torch.matmul(x, hcopies[i % n16], out=y))
+        rows.append(dict(M=M, w4a16_us=round(t_q, 2), fp16_us=round(t_h, 2), speedup=round(t_h / t_q, 3)))
+        log("K=%d N=%d M=%5d  W4A16 %9.2f us  fp16 hipBLASLt %9.2f us  speedup %.2fx" % (K, N, M, t_q, t_h, t_h / t_q))
+    return rows
 
 
 def build_points(configs):
@@ -206,8 +315,29 @@ def main():
     ap.add_argument("--ingest-pmc", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
                     help="turn rocprofv3 FETCH_SIZE / WRITE_SIZE runs of one step (--steps 1 --warmup 0) and "
                          "of --copy-calibration into the stored HBM traffic of the dominant kernel")
-    ap.add_argument("--dominant", default="tiled_kernel<128,32>", help="kernel name for --ingest-pmc")
+    ap.add_argument("--dominant", default="tiled_kernel<128,32>", help="kernel name for --ingest-pmc/--ingest-trace")
+    ap.add_argument("--compare-fp16", action="store_true",
+                    help="only compare the W4A16 GEMM with an fp16 GEMM through torch (hipBLASLt) on the "
+                         "8192x8192 Llama-2-70B o_proj shape over M (context, not the metric)")
+    ap.add_argument("--ingest-trace", metavar="KERNEL_TRACE_CSV",
+                    help="per-GEMM kernel durations from a rocprofv3 --kernel-trace run of this script")
+    ap.add_argument("--trace-out", default=os.path.join(ROOT, "profiles", "bench_llama2_7b_70b_kernel_trace.md"))
+    ap.add_argument("--trace-command", default="rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o kt "
+                    "-- python3 <repo>/bench.py --steps 5 --warmup 2 --no-cpu-baseline")
     args = ap.parse_args()
+
+    if args.ingest_trace:
+        import paper_2402_10076_amd as Q
+        import workloads as W
+        points = build_points([int(c) for c in args.configs.split(",") if c])
+        for p in points:
+            p["sel"] = Q.select_config(p["M"], p["N"], p["K"])
+            p["kernel"] = kernel_name(p["sel"])
+            p["bytes"] = W.alg_bytes(p["M"], p["N"], p["K"])
+            p["flops"] = W.flops(p["M"], p["N"], p["K"])
+        print("dominant %s mean kernel duration %.2f us" % (
+            args.dominant, ingest_trace(args.ingest_trace, points, args.dominant, args.trace_out, args.trace_command)))
+        return
 
     if args.ingest_pmc:
         import paper_2402_10076_amd as Q
@@ -239,6 +369,10 @@ def main():
         sys.exit(1)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.compare_fp16:
+        rows = compare_fp16(8192, 8192, [1, 4, 16, 32, 64, 128, 256, 512, 1024, 2048])
+        print(json.dumps({"compare": "w4a16 vs fp16 hipBLASLt", "K": 8192, "N": 8192, "rows": rows}))
         return
     Q.lib()  # raises if the HIP library is not built
 
