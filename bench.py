@@ -319,12 +319,23 @@ def main():
     ap.add_argument("--compare-fp16", action="store_true",
                     help="only compare the W4A16 GEMM with an fp16 GEMM through torch (hipBLASLt) on the "
                          "8192x8192 Llama-2-70B o_proj shape over M (context, not the metric)")
+    ap.add_argument("--tune", action="store_true",
+                    help="autotune every GEMM shape of the step during setup (untimed) before timing")
+    ap.add_argument("--tune-save", default="", help="with --tune: write the tune table here")
+    ap.add_argument("--tune-table", default=os.path.join(ROOT, "paper_2402_10076_amd", "tune_mi355x.txt"),
+                    help="tune table loaded before planning (default: the library's MI355X table for the "
+                         "bench shapes, written by --tune --tune-save)")
+    ap.add_argument("--no-tune-table", action="store_true", help="plan with the built-in rules only")
     ap.add_argument("--ingest-trace", metavar="KERNEL_TRACE_CSV",
                     help="per-GEMM kernel durations from a rocprofv3 --kernel-trace run of this script")
     ap.add_argument("--trace-out", default=os.path.join(ROOT, "profiles", "bench_llama2_7b_70b_kernel_trace.md"))
     ap.add_argument("--trace-command", default="rocprofv3 --kernel-trace --stats --output-format csv -d <dir> -o kt "
                     "-- python3 <repo>/bench.py --steps 5 --warmup 2 --no-cpu-baseline")
     args = ap.parse_args()
+
+    if args.tune_table and not args.no_tune_table and not args.tune:
+        import paper_2402_10076_amd as Q
+        Q.tune_table_load(args.tune_table)
 
     if args.ingest_trace:
         import paper_2402_10076_amd as Q
@@ -401,12 +412,16 @@ def main():
         p["w"] = tuple(t.clone() for t in base)
         p["x"] = xd[:p["M"]]
         p["y"] = torch.empty((p["M"], p["N"]), dtype=torch.float16, device=dev)
+        if args.tune:
+            Q.tune(p["x"], *p["w"], p["N"], y=p["y"])
         p["sel"] = Q.select_config(p["M"], p["N"], p["K"])
         p["kernel"] = kernel_name(p["sel"])
         p["flops"] = W.flops(p["M"], p["N"], p["K"])
         p["bytes"] = W.alg_bytes(p["M"], p["N"], p["K"])
     xs.clear()
     torch.cuda.synchronize()
+    if args.tune and args.tune_save:
+        Q.tune_table_save(args.tune_save)
     log("setup %.1f s, %d GEMMs per step, %.2f GB of packed weights on device" % (
         time.perf_counter() - t_setup, len(points),
         sum(sum(t.numel() * t.element_size() for t in p["w"]) for p in points) / 1e9))
@@ -561,6 +576,9 @@ def main():
         },
         "hbm_gbps": round(tot_bytes * args.steps / elapsed / 1e9, 1),
         "timing": "K replays of a HIP graph of the step; per-GEMM times from HIP events in eager steps",
+        "plan": ("autotuned at setup" if args.tune else
+                 "built-in rules" if args.no_tune_table or not args.tune_table else
+                 "tune table " + os.path.basename(args.tune_table)),
         "events_ms_per_step": round(sum(p["ms"] for p in points), 4),
         "roofline": roof,
         "roofline_small_m": dict(bound="hbm", achieved=round(s_gbs, 1), peak=HBM_PEAK_GBS, unit="GB/s",

@@ -41,6 +41,7 @@ extern "C" {
 #define QUICK_ERR_ALIGNMENT 5    /* device pointer not aligned (see below)   */
 #define QUICK_ERR_HIP 6          /* HIP runtime error (launch, allocation)   */
 #define QUICK_ERR_WORKSPACE 7    /* caller workspace missing or too small    */
+#define QUICK_ERR_IO 8           /* tune table file unreadable / malformed   */
 
 /* Human-readable name of a status code (static storage, never NULL). */
 const char* quick_status_string(int status);
@@ -148,6 +149,35 @@ size_t quick_workspace_bytes(int64_t M, int64_t N, int64_t K, const quick_config
 /* The configuration the automatic heuristic picks for a shape (for logs and
  * benchmarks).  Errors: INVALID_ARG (NULL cfg), SHAPE. */
 int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config_t* cfg);
+
+/* ---- per-shape autotuning (the paper leaves split-K / tile choice as a
+ * tuning knob; Section 5 names autotuning as future work) ---------------- */
+
+/* Times every supported kernel configuration for this shape on the caller's
+ * buffers (same arguments and contract as quick_w4a16_gemm; y is
+ * overwritten, the last write coming from the best configuration) with HIP
+ * events on `stream`, and records the fastest in the process-wide tune
+ * table, keyed by (M, N, K).  From then on quick_w4a16_gemm, and the
+ * automatic choice of quick_w4a16_gemm_ex / quick_workspace_bytes /
+ * quick_select_config, use the recorded configuration for that shape on
+ * every device.  Blocking: synchronizes `stream`; takes a few milliseconds
+ * to a few hundred for large shapes; may grow the internal workspace, so
+ * not for use under graph capture.  `best` (may be NULL) receives the
+ * configuration recorded.  M == 0 records nothing.
+ * Errors: as quick_w4a16_gemm. */
+int quick_tune(const void* x, const void* packed, const void* scales, const void* zeros, void* y,
+               int64_t M, int64_t N, int64_t K, int64_t group, void* stream, quick_config_t* best);
+
+/* Persist / restore the tune table as text: a header line "quick-tune 1"
+ * then one line "M N K variant split_k tile_m tile_n" per shape.  Loading
+ * validates every line first and then merges (later entries replace
+ * earlier ones for the same shape); on any malformed line nothing is loaded.
+ * Errors: INVALID_ARG (NULL path), IO (cannot open / malformed). */
+int quick_tune_table_save(const char* path);
+int quick_tune_table_load(const char* path);
+/* Number of shapes in the tune table; quick_tune_table_clear empties it. */
+int quick_tune_table_size(void);
+void quick_tune_table_clear(void);
 
 #ifdef __cplusplus
 }

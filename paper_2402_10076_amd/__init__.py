@@ -35,6 +35,7 @@ QUICK_ERR_RANGE = 4
 QUICK_ERR_ALIGNMENT = 5
 QUICK_ERR_HIP = 6
 QUICK_ERR_WORKSPACE = 7
+QUICK_ERR_IO = 8
 
 VARIANT_AUTO = 0
 VARIANT_STREAM = 1
@@ -92,6 +93,16 @@ def lib():
             L.quick_workspace_bytes.restype = SZ
             L.quick_select_config.argtypes = [I64, I64, I64, ctypes.POINTER(QuickConfig)]
             L.quick_select_config.restype = I
+            L.quick_tune.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P, ctypes.POINTER(QuickConfig)]
+            L.quick_tune.restype = I
+            L.quick_tune_table_save.argtypes = [ctypes.c_char_p]
+            L.quick_tune_table_save.restype = I
+            L.quick_tune_table_load.argtypes = [ctypes.c_char_p]
+            L.quick_tune_table_load.restype = I
+            L.quick_tune_table_size.argtypes = []
+            L.quick_tune_table_size.restype = I
+            L.quick_tune_table_clear.argtypes = []
+            L.quick_tune_table_clear.restype = None
             _lib = L
     return _lib
 
@@ -212,8 +223,41 @@ def w4a16_gemm(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zero
     return y
 
 
+def tune(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor, N: int,
+         y: torch.Tensor | None = None, group: int = 128, stream=None) -> dict:
+    """Time every configuration for this shape on these buffers and record the
+    fastest in the library's tune table (quick_tune); returns it."""
+    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
+        raise QuickError(QUICK_ERR_INVALID_ARG, "tune: x must be a contiguous [M][K] float16 tensor")
+    M, K = x.shape
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    c = QuickConfig()
+    _check(lib().quick_tune(_dptr(x), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y), M, N, K, group,
+                            ctypes.c_void_p(st.cuda_stream), ctypes.byref(c)), "quick_tune")
+    return c.as_dict()
+
+
+def tune_table_save(path: str) -> None:
+    _check(lib().quick_tune_table_save(os.fsencode(path)), "quick_tune_table_save")
+
+
+def tune_table_load(path: str) -> None:
+    _check(lib().quick_tune_table_load(os.fsencode(path)), "quick_tune_table_load")
+
+
+def tune_table_size() -> int:
+    return int(lib().quick_tune_table_size())
+
+
+def tune_table_clear() -> None:
+    lib().quick_tune_table_clear()
+
+
 EXPORTED = (
     "quick_status_string", "quick_pack_format_version", "quick_packed_sizes", "quick_pack_weights",
     "quick_unpack_weights", "quick_w4a16_gemm", "quick_w4a16_gemm_ex", "quick_workspace_bytes",
-    "quick_select_config",
+    "quick_select_config", "quick_tune", "quick_tune_table_save", "quick_tune_table_load",
+    "quick_tune_table_size", "quick_tune_table_clear",
 )

@@ -28,11 +28,13 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <cstdio>
 #include <cstring>
 #include <map>
 #include <mutex>
 #include <type_traits>
 #include <utility>
+#include <vector>
 
 #include "quick.h"
 #include "quick_internal.h"
@@ -887,6 +889,26 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
     return QUICK_OK;
 }
 
+// ---- tune table: shape -> configuration measured fastest by quick_tune
+struct ShapeKey {
+    int64_t M, N, K;
+    bool operator<(const ShapeKey& o) const
+    {
+        return M != o.M ? M < o.M : N != o.N ? N < o.N : K < o.K;
+    }
+};
+std::mutex g_tune_mu;
+std::map<ShapeKey, quick_config_t> g_tune;
+
+bool tuned_config(int64_t M, int64_t N, int64_t K, quick_config_t* out)
+{
+    std::lock_guard<std::mutex> lk(g_tune_mu);
+    auto it = g_tune.find(ShapeKey{M, N, K});
+    if (it == g_tune.end()) return false;
+    *out = it->second;
+    return true;
+}
+
 bool tiled_supported(int bm, int wn)
 {
     return ((bm == 16 || bm == 32) && (wn == 16 || wn == 32)) || (bm == 64 && wn == 32) ||
@@ -896,6 +918,8 @@ bool tiled_supported(int bm, int wn)
 int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* pl)
 {
     auto_plan(M, N, K, pl);
+    quick_config_t tuned;
+    if (!cfg && tuned_config(M, N, K, &tuned)) cfg = &tuned;
     if (!cfg) return QUICK_OK;
     const int64_t KG = K / 128;
     if (cfg->variant < 0 || cfg->variant > 3 || cfg->split_k < 0) return QUICK_ERR_INVALID_ARG;
@@ -1206,11 +1230,147 @@ extern "C" int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config
     if (!cfg) return QUICK_ERR_INVALID_ARG;
     if (M < 0 || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return QUICK_ERR_SHAPE;
     Plan pl;
-    auto_plan(M, N, K, &pl);
+    if (make_plan(M, N, K, nullptr, &pl) != QUICK_OK) auto_plan(M, N, K, &pl);
     finish_plan(M, N, K, &pl);
     cfg->variant = pl.variant;
     cfg->split_k = pl.split;
     cfg->tile_m = is_tiled(pl.variant) ? pl.bm : 0;
     cfg->tile_n = pl.wn;
     return QUICK_OK;
+}
+
+namespace {
+
+// Configurations worth timing for a shape: the stream kernel (small M), the
+// tiled tiles no taller than the next power of two >= M (at least 16) with
+// splits 1, 2, 4, 8 (each slice keeping >= 2 k-groups), and stream-K.
+std::vector<quick_config_t> tune_candidates(int64_t M, int64_t K)
+{
+    std::vector<quick_config_t> c;
+    const int64_t KG = K / 128;
+    if (M <= 64)
+        for (int w : {1, 2, 4, 8})
+            for (int p : {1, 2}) c.push_back(quick_config_t{kVariantStream, w, 0, p});
+    int64_t mcap = 16;
+    while (mcap < M && mcap < 128) mcap *= 2;
+    static const int tiles[][2] = {{16, 16}, {16, 32}, {32, 16}, {32, 32}, {64, 32}, {64, 64}, {128, 32}};
+    for (const auto& t : tiles) {
+        if (t[0] > mcap) continue;
+        for (int s : {1, 2, 4, 8})
+            if (s == 1 || KG / s >= 2) c.push_back(quick_config_t{kVariantTiled, s, t[0], t[1]});
+        c.push_back(quick_config_t{kVariantStreamK, 0, t[0], t[1]});
+    }
+    return c;
+}
+
+}  // namespace
+
+extern "C" int quick_tune(const void* x, const void* packed, const void* scales, const void* zeros, void* y,
+                          int64_t M, int64_t N, int64_t K, int64_t group, void* stream, quick_config_t* best)
+{
+    int st = validate(x, packed, scales, zeros, y, M, N, K, group);
+    if (st) return st;
+    if (M == 0) return QUICK_OK;
+    hipStream_t hs = (hipStream_t)stream;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+        if (e0) (void)hipEventDestroy(e0);
+        return QUICK_ERR_HIP;
+    }
+    constexpr int kReps = 5;
+    float best_ms = 0.f;
+    quick_config_t bestc{};
+    bool found = false;
+    for (const quick_config_t& c : tune_candidates(M, K)) {
+        st = gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, &c, nullptr, 0);  // warm-up
+        if (st == QUICK_ERR_INVALID_ARG) continue;  // not supported for this shape
+        if (st) break;
+        float ms = 0.f;
+        if (hipEventRecord(e0, hs) != hipSuccess) { st = QUICK_ERR_HIP; break; }
+        for (int r = 0; r < kReps && !st; ++r)
+            st = gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, &c, nullptr, 0);
+        if (st) break;
+        if (hipEventRecord(e1, hs) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+            hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
+            st = QUICK_ERR_HIP;
+            break;
+        }
+        if (!found || ms < best_ms) {
+            best_ms = ms;
+            bestc = c;
+            found = true;
+        }
+    }
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    if (st) return st;
+    if (!found) return QUICK_ERR_INVALID_ARG;
+    {
+        std::lock_guard<std::mutex> lk(g_tune_mu);
+        g_tune[ShapeKey{M, N, K}] = bestc;
+    }
+    // leave y holding the chosen configuration's result
+    st = gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, &bestc, nullptr, 0);
+    if (st) return st;
+    if (best) *best = bestc;
+    return QUICK_OK;
+}
+
+extern "C" int quick_tune_table_save(const char* path)
+{
+    if (!path) return QUICK_ERR_INVALID_ARG;
+    std::lock_guard<std::mutex> lk(g_tune_mu);
+    FILE* f = std::fopen(path, "w");
+    if (!f) return QUICK_ERR_IO;
+    bool ok = std::fprintf(f, "quick-tune 1\n") > 0;
+    for (const auto& e : g_tune)
+        ok = ok && std::fprintf(f, "%lld %lld %lld %d %d %d %d\n", (long long)e.first.M, (long long)e.first.N,
+                                (long long)e.first.K, e.second.variant, e.second.split_k, e.second.tile_m,
+                                e.second.tile_n) > 0;
+    ok = (std::fclose(f) == 0) && ok;
+    return ok ? QUICK_OK : QUICK_ERR_IO;
+}
+
+extern "C" int quick_tune_table_load(const char* path)
+{
+    if (!path) return QUICK_ERR_INVALID_ARG;
+    FILE* f = std::fopen(path, "r");
+    if (!f) return QUICK_ERR_IO;
+    char line[256];
+    bool ok = std::fgets(line, sizeof line, f) && std::strncmp(line, "quick-tune 1", 12) == 0;
+    std::vector<std::pair<ShapeKey, quick_config_t>> rows;
+    while (ok && std::fgets(line, sizeof line, f)) {
+        long long m, n, k;
+        quick_config_t c{};
+        char extra;
+        const int got = std::sscanf(line, "%lld %lld %lld %d %d %d %d %c", &m, &n, &k, &c.variant, &c.split_k,
+                                    &c.tile_m, &c.tile_n, &extra);
+        if (got != 7 || m <= 0 || n <= 0 || k <= 0 || k % 128 != 0 || n % 16 != 0) {
+            ok = false;
+            break;
+        }
+        Plan pl;
+        if (make_plan(m, n, k, &c, &pl) != QUICK_OK) {
+            ok = false;
+            break;
+        }
+        rows.push_back({ShapeKey{m, n, k}, c});
+    }
+    std::fclose(f);
+    if (!ok) return QUICK_ERR_IO;
+    std::lock_guard<std::mutex> lk(g_tune_mu);
+    for (const auto& r : rows) g_tune[r.first] = r.second;
+    return QUICK_OK;
+}
+
+extern "C" int quick_tune_table_size(void)
+{
+    std::lock_guard<std::mutex> lk(g_tune_mu);
+    return (int)g_tune.size();
+}
+
+extern "C" void quick_tune_table_clear(void)
+{
+    std::lock_guard<std::mutex> lk(g_tune_mu);
+    g_tune.clear();
 }

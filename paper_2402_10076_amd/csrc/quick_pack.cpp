@@ -170,6 +170,7 @@ extern "C" const char* quick_status_string(int status)
     case QUICK_ERR_ALIGNMENT: return "QUICK_ERR_ALIGNMENT: device pointer misaligned";
     case QUICK_ERR_HIP: return "QUICK_ERR_HIP: HIP runtime error";
     case QUICK_ERR_WORKSPACE: return "QUICK_ERR_WORKSPACE: workspace missing or too small";
+    case QUICK_ERR_IO: return "QUICK_ERR_IO: tune table file unreadable or malformed";
     default: return "unknown quick status";
     }
 }

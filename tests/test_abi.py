@@ -130,6 +130,40 @@ def test_select_config_regimes():
 
 
 def test_status_strings():
-    for st in range(8):
+    for st in range(9):
         assert Q.status_string(st).startswith("QUICK_")
     assert "unknown" in Q.status_string(99)
+
+
+def test_tune_table_load_select_save(tmp_path):
+    """A loaded tune table drives the automatic choice; save writes it back
+    unchanged; a malformed file loads nothing."""
+    Q.tune_table_clear()
+    try:
+        good = tmp_path / "t.txt"
+        good.write_text("quick-tune 1\n256 4096 4096 2 4 64 32\n1 8192 8192 1 2 0 2\n"
+                        "300 528 2304 3 24 64 32\n")
+        Q.tune_table_load(str(good))
+        assert Q.tune_table_size() == 3
+        assert Q.select_config(256, 4096, 4096) == dict(variant=2, split_k=4, tile_m=64, tile_n=32)
+        assert Q.select_config(1, 8192, 8192) == dict(variant=1, split_k=2, tile_m=0, tile_n=2)
+        assert Q.select_config(300, 528, 2304)["variant"] == 3
+        # the tuned split-K shape now needs its workspace in the automatic path too
+        assert Q.workspace_bytes(256, 4096, 4096) == Q.WS_COUNTER_BYTES + 4 * 256 * 4096 * 4
+        out = tmp_path / "u.txt"
+        Q.tune_table_save(str(out))
+        lines = out.read_text().splitlines()
+        assert lines[0] == "quick-tune 1" and sorted(lines[1:]) == sorted(good.read_text().splitlines()[1:])
+        for bad in ("quick-tune 2\n", "quick-tune 1\n256 4096 4096 2 4 64\n",
+                    "quick-tune 1\n256 4096 4096 2 4 96 32\n", "quick-tune 1\n256 4096 4000 2 4 64 32\n",
+                    "quick-tune 1\n1 2 3 4 5 6 7 8\n"):
+            Q.tune_table_clear()
+            f = tmp_path / "bad.txt"
+            f.write_text(bad)
+            with pytest.raises(Q.QuickError):
+                Q.tune_table_load(str(f))
+            assert Q.tune_table_size() == 0
+        with pytest.raises(Q.QuickError):
+            Q.tune_table_load(str(tmp_path / "missing.txt"))
+    finally:
+        Q.tune_table_clear()
