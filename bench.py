@@ -308,7 +308,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--configs", default="2,5", help="workload configs (2 = Llama-2-7B, 5 = Llama-2-70B)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-col-fraction", type=float, default=1.0 / 32)
+    ap.add_argument("--cpu-col-fraction", type=float, default=1.0 / 8)
     ap.add_argument("--points-out", default="", help="optional path for the per-GEMM table (JSON)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain %d MiB device copy (scales rocprofv3 byte counters)" % (COPY_CAL_BYTES >> 20))
