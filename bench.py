@@ -72,7 +72,7 @@ def launch_sequence(points):
         if sel["variant"] == 1:
             seq.append((p["kernel"], "stream_kernel<"))
         else:
-            seq.append((p["kernel"], "tiled_kernel<%d, %d>" % (sel["tile_m"], sel["tile_n"])))
+            seq.append((p["kernel"], "tiled_kernel<%d, %d, 0>" % (sel["tile_m"], sel["tile_n"])))
             if sel["variant"] == 2 and sel["split_k"] > 1:
                 seq.append((None, "splitk_reduce_kernel"))
     return seq
@@ -264,6 +264,45 @@ def compare_fp16(K, N, Ms, reps=20):
     return rows
 
 
+def ablation(shapes, reps=20):
+    """The method's central choice measured: the same 64 x 256 tiled kernel
+    with the dequantized weights going straight to the fragment registers
+    (mode 0) or through an LDS tile and back (mode 1 padded rows, mode 2
+    unpadded rows); HIP events over `reps` back-to-back launches rotating
+    through >= 1 GiB of weight copies."""
+    import torch
+    import paper_2402_10076_amd as Q
+    import workloads as W
+    rows = []
+    for K, N, Ms in shapes:
+        q, z, s = W.draw_weights(5, 2, K, N)
+        wq = Q.to_device(*Q.pack_weights(q, z, s))
+        nq = max(2, -(-(1 << 30) // (K * N // 2)))
+        copies = [tuple(t.clone() for t in wq) for _ in range(nq)]
+        for M in Ms:
+            x = torch.randn(M, K, device="cuda").half()
+            y = torch.empty(M, N, device="cuda", dtype=torch.float16)
+            t = []
+            for mode in (0, 1, 2):
+                for i in range(3):
+                    Q.ablation_gemm(x, *copies[i % nq], N, mode, y=y)
+                torch.cuda.synchronize()
+                torch.cuda._sleep(5_000_000)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for i in range(reps):
+                    Q.ablation_gemm(x, *copies[i % nq], N, mode, y=y)
+                e1.record()
+                torch.cuda.synchronize()
+                t.append(e0.elapsed_time(e1) / reps * 1e3)
+            rows.append(dict(K=K, N=N, M=M, direct_us=round(t[0], 2), writeback_padded_us=round(t[1], 2),
+                             writeback_unpadded_us=round(t[2], 2)))
+            log("K=%5d N=%5d M=%5d  direct %8.2f us  write-back padded %8.2f us (%.2fx)  unpadded %8.2f us (%.2fx)"
+                % (K, N, M, t[0], t[1], t[1] / t[0], t[2], t[2] / t[0]))
+        del copies
+    return rows
+
+
 def build_points(configs):
     import workloads as W
     pts = []
@@ -326,6 +365,10 @@ def main():
                     help="tune table loaded before planning (default: the library's MI355X table for the "
                          "bench shapes, written by --tune --tune-save)")
     ap.add_argument("--no-tune-table", action="store_true", help="plan with the built-in rules only")
+    ap.add_argument("--ablation", action="store_true",
+                    help="only measure direct-to-register vs LDS write-back of the dequantized weights")
+    ap.add_argument("--ablation-only", default="", metavar="K,N,M",
+                    help="with --ablation: one shape, 5 launches per mode (for counter runs)")
     ap.add_argument("--ingest-trace", metavar="KERNEL_TRACE_CSV",
                     help="per-GEMM kernel durations from a rocprofv3 --kernel-trace run of this script")
     ap.add_argument("--trace-out", default=os.path.join(ROOT, "profiles", "bench_llama2_7b_70b_kernel_trace.md"))
@@ -380,6 +423,15 @@ def main():
         sys.exit(1)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.ablation:
+        if args.ablation_only:
+            K, N, M = (int(v) for v in args.ablation_only.split(","))
+            rows = ablation([(K, N, [M])], reps=5)
+        else:
+            rows = ablation([(8192, 8192, [16, 64, 256, 1024]), (8192, 57344, [256, 1024]),
+                             (28672, 8192, [256, 1024]), (4096, 4096, [256])])
+        print(json.dumps({"ablation": "direct-to-register vs LDS write-back (64x256 tiles)", "rows": rows}))
         return
     if args.compare_fp16:
         rows = compare_fp16(8192, 8192, [1, 4, 16, 32, 64, 128, 256, 512, 1024, 2048])

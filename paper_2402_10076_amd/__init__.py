@@ -103,6 +103,8 @@ def lib():
             L.quick_tune_table_size.restype = I
             L.quick_tune_table_clear.argtypes = []
             L.quick_tune_table_clear.restype = None
+            L.quick_ablation_gemm.argtypes = [P, P, P, P, P, I64, I64, I64, I, P]
+            L.quick_ablation_gemm.restype = I
             _lib = L
     return _lib
 
@@ -239,6 +241,19 @@ def tune(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zeros: tor
     return c.as_dict()
 
 
+def ablation_gemm(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor,
+                  N: int, mode: int, y: torch.Tensor | None = None) -> torch.Tensor:
+    """quick_ablation_gemm: mode 0 direct-to-register (the method), 1 / 2
+    write-back through LDS with padded / unpadded rows."""
+    M, K = x.shape
+    if y is None:
+        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
+    st = torch.cuda.current_stream(x.device)
+    _check(lib().quick_ablation_gemm(_dptr(x), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y), M, N, K,
+                                     mode, ctypes.c_void_p(st.cuda_stream)), "quick_ablation_gemm")
+    return y
+
+
 def tune_table_save(path: str) -> None:
     _check(lib().quick_tune_table_save(os.fsencode(path)), "quick_tune_table_save")
 
@@ -259,5 +274,5 @@ EXPORTED = (
     "quick_status_string", "quick_pack_format_version", "quick_packed_sizes", "quick_pack_weights",
     "quick_unpack_weights", "quick_w4a16_gemm", "quick_w4a16_gemm_ex", "quick_workspace_bytes",
     "quick_select_config", "quick_tune", "quick_tune_table_save", "quick_tune_table_load",
-    "quick_tune_table_size", "quick_tune_table_clear",
+    "quick_tune_table_size", "quick_tune_table_clear", "quick_ablation_gemm",
 )

@@ -37,6 +37,7 @@
 #include <vector>
 
 #include "quick.h"
+#include "quick_ablation.h"
 #include "quick_internal.h"
 
 namespace {
@@ -434,7 +435,12 @@ constexpr size_t kSkCounterBytes = QUICK_WORKSPACE_COUNTER_BYTES;
 static_assert(kSkCounterBytes >= kSkMaxWorkgroups * sizeof(unsigned), "one counter per workgroup");
 constexpr int kCoherentAux = 0x11;  // sc0 sc1: coherent across XCDs, write-through
 
-template <int BM, int WN>
+// WB != 0 builds the write-back ablation of the conventional design (the
+// dequantized weights go through an LDS tile and are read back as matrix
+// fragments): 1 = rows padded by 16 bytes (conflict-free), 2 = unpadded
+// [n][k] rows (same-bank fragment accesses).  Only the ablation library
+// launches it; WB = 0 is the method's direct-to-register path.
+template <int BM, int WN, int WB = 0>
 __global__ void __launch_bounds__(64 * kTiledWaves, 1)
 tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
              const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
@@ -464,6 +470,10 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     auto stage_ptr = [&](int st) -> uint8_t* {
         return st == 0 ? lds_s0 : st == 1 ? lds_s1 : st == 2 ? lds_s2 : lds_s3;
     };
+    // write-back ablation: per wave an [NP*16 columns][128 channels] f16 tile
+    constexpr int WB_RS = WB == 1 ? 136 : 128;   // row stride in halves
+    constexpr int WB_BYTES = WB ? WAVES * NP * 16 * WB_RS * 2 : 16;
+    __shared__ __attribute__((aligned(16))) uint8_t lds_wb[WB_BYTES];
 
     const int KG = K >> 7;
     const int NT = N >> 4;
@@ -547,14 +557,31 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         return bits_as<h8_t>(*reinterpret_cast<const u4_t*>(src));
     };
 
+    // write-back ablation: this lane's 8 channels of step j, column 16p + c
+    auto wb_at = [&](int p, int j) -> uint8_t* {
+        return lds_wb + ((size_t)(wave * NP * 16 + p * 16 + c) * WB_RS + 32 * j + 8 * g) * 2;
+    };
     auto kgroup = [&](int st) __attribute__((always_inline)) {
         Deq d[NP];
 #pragma unroll
         for (int p = 0; p < NP; ++p) d[p] = make_deq(sr[st][p], (zr[st][p] >> (4 * (c & 7))) & 15u);
         h8_t a[2][NP];
         h8_t b[2][MTT];
+        if constexpr (WB != 0) {
+            // the conventional order: dequantize the whole k-group of weights
+            // into the LDS tile first (same-wave LDS operations stay ordered)
 #pragma unroll
-        for (int p = 0; p < NP; ++p) a[0][p] = dequant8(wr[st][p][0], d[p]);
+            for (int p = 0; p < NP; ++p)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    *reinterpret_cast<h8_t*>(wb_at(p, j)) = dequant8(wr[st][p][j], d[p]);
+        }
+        auto afrag = [&](int p, int j) -> h8_t {
+            if constexpr (WB != 0) return *reinterpret_cast<const h8_t*>(wb_at(p, j));
+            else return dequant8(wr[st][p][j], d[p]);
+        };
+#pragma unroll
+        for (int p = 0; p < NP; ++p) a[0][p] = afrag(p, 0);
 #pragma unroll
         for (int mt = 0; mt < MTT; ++mt) b[0][mt] = bfrag(st, mt, 0);
 #pragma unroll
@@ -568,7 +595,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
             }
             if (j < 3) {
 #pragma unroll
-                for (int p = 0; p < NP; ++p) a[nx][p] = dequant8(wr[st][p][j + 1], d[p]);
+                for (int p = 0; p < NP; ++p) a[nx][p] = afrag(p, j + 1);
                 constexpr int VPER = (13 * NP + MTT - 1) / MTT;  // dequant VALU ops per block
 #pragma unroll
                 for (int mt = 0; mt < MTT; ++mt) {
@@ -1373,4 +1400,31 @@ extern "C" void quick_tune_table_clear(void)
 {
     std::lock_guard<std::mutex> lk(g_tune_mu);
     g_tune.clear();
+}
+
+// Ablation of the method's central choice (declared in quick_ablation.h): the
+// 64 x 256 data-parallel tiled kernel with the dequantized weights going
+// straight to the matrix-instruction registers (mode 0, the method) or
+// through an LDS tile and back (mode 1 padded rows, mode 2 unpadded rows).
+extern "C" int quick_ablation_gemm(const void* x, const void* packed, const void* scales, const void* zeros,
+                                   void* y, int64_t M, int64_t N, int64_t K, int mode, void* stream)
+{
+    int st = validate(x, packed, scales, zeros, y, M, N, K, 128);
+    if (st) return st;
+    if (mode < 0 || mode > 2) return QUICK_ERR_INVALID_ARG;
+    if (M == 0) return QUICK_OK;
+    const int nm = ceil_div(M, 64), nn = ceil_div(N, kTiledWaves * 32);
+    const int grid = ceil_div((int64_t)nm * nn, 8) * 8;
+    const int KG = (int)(K / 128);
+    auto args = [&](auto kern) {
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * kTiledWaves), 0, (hipStream_t)stream,
+                           static_cast<const uint16_t*>(x), static_cast<const u4_t*>(packed),
+                           static_cast<const uint16_t*>(scales), static_cast<const uint32_t*>(zeros),
+                           static_cast<uint16_t*>(y), (float*)nullptr, (int)M, (int)N, (int)K, KG, nm, nn, 1);
+    };
+    (void)hipGetLastError();
+    if (mode == 0) args(tiled_kernel<64, 32, 0>);
+    else if (mode == 1) args(tiled_kernel<64, 32, 1>);
+    else args(tiled_kernel<64, 32, 2>);
+    return hipGetLastError() == hipSuccess ? QUICK_OK : QUICK_ERR_HIP;
 }

@@ -1,5 +1,5 @@
 """The C ABI without a GPU: the library loads, exports every function that
-include/quick.h declares, the header compiles as plain C, and every
+include/*.h declare, the headers compile as plain C, and every
 validation path returns its status before touching the device."""
 import ctypes
 import os
@@ -13,13 +13,16 @@ import pytest
 import paper_2402_10076_amd as Q
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "quick.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in sorted(os.listdir(os.path.join(ROOT, "include")))
+           if h.endswith(".h")]
 
 
 def declared_functions():
-    src = open(HEADER).read()
-    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(quick_[a-z0-9_]+)\s*\(", src)))
+    names = set()
+    for h in HEADERS:
+        src = re.sub(r"/\*.*?\*/", "", open(h).read(), flags=re.S)
+        names |= set(re.findall(r"\b(quick_[a-z0-9_]+)\s*\(", src))
+    return sorted(names)
 
 
 def test_every_declared_symbol_is_exported():
@@ -34,6 +37,7 @@ def test_every_declared_symbol_is_exported():
 def test_header_is_plain_c_and_links():
     prog = r'''
 #include "quick.h"
+#include "quick_ablation.h"
 #include <stdio.h>
 #include <string.h>
 int main(void) {
@@ -46,6 +50,7 @@ int main(void) {
     memset(&cfg, 0, sizeof cfg);
     if (quick_select_config(1, 4096, 4096, &cfg) != QUICK_OK || cfg.variant != 1) return 5;
     if (quick_w4a16_gemm(0, 0, 0, 0, 0, 0, 4096, 4096, 128, 0) != QUICK_OK) return 6;
+    if (quick_ablation_gemm(0, 0, 0, 0, 0, 4, 4096, 4096, 3, 0) != QUICK_ERR_INVALID_ARG) return 7;
     printf("%s\n", quick_status_string(QUICK_ERR_SHAPE));
     return 0;
 }
