@@ -89,6 +89,16 @@ def read_counter_csv(path: str, counter: str):
     return rows
 
 
+def whole_repetitions(names, seq):
+    """How many times the launch sequence `seq` repeats at the start of the
+    dispatched kernel `names`."""
+    reps = 0
+    while (reps + 1) * len(seq) <= len(names) and all(
+            prefix in names[reps * len(seq) + i] for i, (_, prefix) in enumerate(seq)):
+        reps += 1
+    return reps
+
+
 def ingest_pmc(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, points, dominant):
     """HBM bytes per launch of the dominant kernel from FETCH_SIZE / WRITE_SIZE
     runs of one bench step, each scaled by what the counter reads for a plain
@@ -98,15 +108,16 @@ def ingest_pmc(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, points, domin
     for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
         ours = [r for r in read_counter_csv(path, name)
                 if "anonymous namespace)::" in r[1] and "at::" not in r[1]]
-        # the run issues the step's launch sequence a whole number of times
-        # (eager warm-up, graph replays, eager timing steps)
-        if not ours or len(ours) % len(seq):
-            raise SystemExit("%s: %d library dispatches, not a multiple of %d" % (path, len(ours), len(seq)))
-        full = seq * (len(ours) // len(seq))
-        for (bname, prefix), r in zip(full, ours):
-            if prefix not in r[1]:
-                raise SystemExit("dispatch %d is %s, expected %s" % (r[0], r[1][:80], prefix))
+        # whole repetitions of the step's launch sequence from the start
+        # (eager warm-up, graph replays, eager timing steps); the subset-graph
+        # replays that follow are not used
+        reps = whole_repetitions([r[1] for r in ours], seq)
+        if reps == 0:
+            raise SystemExit("%s: the library dispatches do not start with the step's launch sequence" % path)
+        full = seq * reps
         vals = [r[2] for (bname, _), r in zip(full, ours) if bname == dominant]
+        if not vals:
+            raise SystemExit("no launch of %s in the step" % dominant)
         per[name] = float(np.mean(vals))
     cal = {}
     for name, path in (("FETCH_SIZE", cal_fetch_csv), ("WRITE_SIZE", cal_write_csv)):
@@ -145,10 +156,7 @@ def ingest_trace(trace_csv, points, dominant, out_md, command):
     # whole repetitions of the step from the start (eager warm-up, graph
     # replays, eager event steps); the subset-graph replays that follow are
     # not used
-    reps = 0
-    while (reps + 1) * len(seq) <= len(rows) and all(
-            prefix in rows[reps * len(seq) + i][1] for i, (_, prefix) in enumerate(seq)):
-        reps += 1
+    reps = whole_repetitions([r[1] for r in rows], seq)
     if reps == 0:
         raise SystemExit("%s: the library dispatches do not start with the step's launch sequence" % trace_csv)
     # per point: its kernels' durations (tiled kernel + reduction when split), per repetition
@@ -190,6 +198,18 @@ def ingest_trace(trace_csv, points, dominant, out_md, command):
         f.write("* Sum of kernel time per step: %.1f us.\n" % tot)
         f.write("* GEMMs with M <= 16: %.1f us of kernels, %.0f GB/s of algorithmic bytes.\n\n" % (s_us, s_gbs))
         f.write("\n".join(lines) + "\n")
+        stats = trace_csv.replace("_kernel_trace.csv", "_kernel_stats.csv")
+        if stats != trace_csv and os.path.exists(stats):
+            # the profiler's own --stats summary of the same run, per kernel symbol
+            # (every launch of the run: warm-up, eager steps, graph replays)
+            f.write("\nrocprofv3 `--stats` summary of the same run (%s), all launches of each "
+                    "kernel symbol:\n\n" % os.path.basename(stats))
+            f.write("| kernel | calls | average us | min us | max us | % of time |\n|---|---|---|---|---|---|\n")
+            for r in csv.DictReader(open(stats)):
+                name = r["Name"].replace("void ", "").replace("(anonymous namespace)::", "").split("(")[0]
+                f.write("| `%s` | %s | %.2f | %.2f | %.2f | %.2f |\n" % (
+                    name, r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3,
+                    float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
     return dom_us
 
 
@@ -354,7 +374,7 @@ def main():
     ap.add_argument("--ingest-pmc", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
                     help="turn rocprofv3 FETCH_SIZE / WRITE_SIZE runs of one step (--steps 1 --warmup 0) and "
                          "of --copy-calibration into the stored HBM traffic of the dominant kernel")
-    ap.add_argument("--dominant", default="tiled_kernel<128,32>", help="kernel name for --ingest-pmc/--ingest-trace")
+    ap.add_argument("--dominant", default="tiled_kernel<128,32>+streamK(G=256)", help="kernel name for --ingest-pmc/--ingest-trace")
     ap.add_argument("--compare-fp16", action="store_true",
                     help="only compare the W4A16 GEMM with an fp16 GEMM through torch (hipBLASLt) on the "
                          "8192x8192 Llama-2-70B o_proj shape over M (context, not the metric)")
