@@ -323,6 +323,102 @@ def ablation(shapes, reps=20):
     return rows
 
 
+def moe(reps=20, sweep=True):
+    """Mixtral-8x7B expert FFN on one GPU (512 tokens, top-2 routing over 8
+    experts, about 128 rows per expert): the 24 expert GEMMs (w1, w3 over the
+    routed tokens, w2 over fresh [M_e][14336] inputs) as 24 dense launches on
+    pre-gathered activations, against 3 grouped launches that gather the
+    token rows inside the kernel.  Each form is one HIP graph, checked against
+    its eager run and timed with HIP events over `reps` replays."""
+    import torch
+    import paper_2402_10076_amd as Q
+    import workloads as W
+    routes = W.mixtral_routing()
+    counts = [len(r) for r in routes]
+    R = sum(counts)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    od = torch.from_numpy(offsets).cuda()
+    rd = torch.from_numpy(np.concatenate(routes).astype(np.int32)).cuda()
+    xt = torch.from_numpy(W.mixtral_tokens().view(np.int16)).cuda().view(torch.float16)
+    xg = [xt[torch.from_numpy(r).cuda()].contiguous() for r in routes]   # gathered outside the GEMMs
+    h = torch.from_numpy(np.concatenate([W.mixtral_w2_input(e, counts[e]) for e in range(8)]).view(np.int16))
+    h = h.cuda().view(torch.float16)
+    mats = []
+    flops = 0
+    for which in range(3):
+        experts = [W.mixtral_expert_weights(e, which) for e in range(8)]
+        K, N = experts[0][0].shape
+        dw, ds, dz = Q.to_device(*Q.pack_experts(experts))
+        wb, zb, sb = Q.packed_sizes(K, N)
+        views = [(dw[e * wb // 4:(e + 1) * wb // 4], ds[e * sb // 2:(e + 1) * sb // 2],
+                  dz[e * zb // 4:(e + 1) * zb // 4]) for e in range(8)]
+        mats.append(dict(K=K, N=N, w=(dw, ds, dz), views=views,
+                         y_dense=torch.empty(R, N, dtype=torch.float16, device="cuda"),
+                         y_grp=torch.empty(R, N, dtype=torch.float16, device="cuda")))
+        flops += 2 * R * N * K
+    stream = torch.cuda.Stream()
+
+    def dense():
+        for which, m in enumerate(mats):
+            for e in range(8):
+                lo, hi = int(offsets[e]), int(offsets[e + 1])
+                x = xg[e] if which < 2 else h[lo:hi]
+                Q.w4a16_gemm(x, *m["views"][e], m["N"], y=m["y_dense"][lo:hi])
+
+    def grouped(cfg):
+        for which, m in enumerate(mats):
+            if which < 2:
+                Q.grouped_gemm(xt, od, *m["w"], m["N"], rows=rd, y=m["y_grp"], cfg=cfg)
+            else:
+                Q.grouped_gemm(h, od, *m["w"], m["N"], y=m["y_grp"], cfg=cfg)
+
+    def timed(fn, outs):
+        with torch.cuda.stream(stream):
+            fn()
+        stream.synchronize()
+        ref = [o.clone() for o in outs]
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            fn()
+        for o in outs:
+            o.zero_()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        with torch.cuda.stream(stream):
+            for _ in range(3):
+                g.replay()
+            e0.record()
+            for _ in range(reps):
+                g.replay()
+            e1.record()
+        torch.cuda.synchronize()
+        if not all(torch.equal(a, b) for a, b in zip(outs, ref)):
+            raise SystemExit("graph replay differs from the eager run")
+        return e0.elapsed_time(e1) / reps * 1e3
+
+    t_dense = timed(dense, [m["y_dense"] for m in mats])
+    rows = [dict(form="24 dense launches (pre-gathered rows)", us=round(t_dense, 2),
+                 tflops=round(flops / t_dense / 1e6, 1))]
+    log("Mixtral 8x7B experts, R=%d routed rows (per expert %s), %.1f GFLOP" % (R, counts, flops / 1e9))
+    log("  24 dense launches        %9.2f us  %7.1f TFLOP/s" % (t_dense, flops / t_dense / 1e6))
+    cfgs = [None]
+    if sweep:
+        for bm, wn in ((64, 32), (128, 32)):
+            cfgs += [Q.make_config(variant=3, tile_m=bm, tile_n=wn)]
+            cfgs += [Q.make_config(variant=2, split_k=s, tile_m=bm, tile_n=wn) for s in (1, 2, 4)]
+    outs = [m["y_grp"] for m in mats]
+    for cfg in cfgs:
+        t = timed(lambda: grouped(cfg), outs)
+        name = "auto %s" % (Q.grouped_select_config(R, 8, mats[0]["N"], mats[0]["K"]),) if cfg is None else \
+            "v%d split %d tile %dx%d" % (cfg.variant, cfg.split_k, cfg.tile_m, cfg.tile_n)
+        diff = max(float((a.float() - b.float()).abs().max() / b.float().abs().max())
+                   for a, b in zip(outs, [m["y_dense"] for m in mats]))
+        rows.append(dict(form="3 grouped launches, " + name, us=round(t, 2), tflops=round(flops / t / 1e6, 1),
+                         speedup=round(t_dense / t, 3), max_rel_diff_vs_dense=round(diff, 6)))
+        log("  3 grouped launches %-40s %9.2f us  %7.1f TFLOP/s  %.2fx  (max rel diff vs dense %.2g)" % (
+            name, t, flops / t / 1e6, t_dense / t, diff))
+    return dict(routed_rows=R, rows_per_expert=counts, gflop=round(flops / 1e9, 2), rows=rows)
+
+
 def build_points(configs):
     import workloads as W
     pts = []
@@ -367,6 +463,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--configs", default="2,5", help="workload configs (2 = Llama-2-7B, 5 = Llama-2-70B)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--moe", action="store_true",
+                    help="time the Mixtral-8x7B expert GEMMs: 24 dense launches vs 3 grouped launches")
+    ap.add_argument("--moe-auto-only", action="store_true", help="with --moe: only the automatic grouped config")
     ap.add_argument("--cpu-col-fraction", type=float, default=1.0 / 8)
     ap.add_argument("--points-out", default="", help="optional path for the per-GEMM table (JSON)")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -452,6 +551,9 @@ def main():
             rows = ablation([(8192, 8192, [16, 64, 256, 1024]), (8192, 57344, [256, 1024]),
                              (28672, 8192, [256, 1024]), (4096, 4096, [256])])
         print(json.dumps({"ablation": "direct-to-register vs LDS write-back (64x256 tiles)", "rows": rows}))
+        return
+    if args.moe:
+        print(json.dumps({"moe": "Mixtral-8x7B expert FFN, dense per expert vs grouped", **moe(sweep=not args.moe_auto_only)}))
         return
     if args.compare_fp16:
         rows = compare_fp16(8192, 8192, [1, 4, 16, 32, 64, 128, 256, 512, 1024, 2048])

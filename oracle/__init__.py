@@ -9,6 +9,8 @@ The arithmetic lives in ``oracle.c`` (plain C, binary64):
 * ``dequant``  -- W = (q - z) * s per group of 128 input channels
   (paper, Section 2.1 and Section 2.3).
 * ``gemm``     -- y = x . W as a naive loop over k in ascending order.
+* ``grouped_gemm`` (Python) -- the mixture-of-experts form: each expert's
+  rows are ``gemm`` of its gathered token rows.
 * ``pack``     -- the QPK16 offline reorder written as its element-wise
   definition (paper, Section 3.2 describes reordering the static weights
   offline to the matrix-instruction operand pattern and to the dequantizer's
@@ -168,6 +170,31 @@ def gemm(x_bits, q, z, s_bits, group: int = 128, cols=None, threads: int = 0) ->
                                  cp, nc, _ptr(y), int(threads))
     if rc:
         raise OracleError("oracle_gemm_f64 failed with status %d" % rc)
+    return y
+
+
+def grouped_gemm(x_bits, rows, offsets, experts, group: int = 128, cols=None, threads: int = 0) -> np.ndarray:
+    """Mixture-of-experts form: routed row r is token row ``rows[r]`` of x
+    (r itself when ``rows`` is None) multiplied by the weights of the expert
+    e with offsets[e] <= r < offsets[e+1].  ``experts``: list of (q, z, s_bits).
+    Each expert's block of rows is :func:`gemm` of its gathered token rows
+    (the per-element definition is the dense GEMM's, Sections 2.1 and 2.3)."""
+    x = _c(x_bits, np.uint16)
+    off = np.asarray(offsets, np.int64)
+    E = len(experts)
+    if off.shape != (E + 1,) or off[0] != 0 or np.any(np.diff(off) < 0):
+        raise OracleError("offsets must be non-decreasing [E+1] starting at 0")
+    R = int(off[-1])
+    r_tok = np.arange(R, dtype=np.int64) if rows is None else np.asarray(rows, np.int64)
+    if r_tok.shape != (R,) or (R and (r_tok.min() < 0 or r_tok.max() >= x.shape[0])):
+        raise OracleError("rows must be [R] token indices of x")
+    N = experts[0][0].shape[1]
+    nc = N if cols is None else len(cols)
+    y = np.zeros((R, nc), np.float64)
+    for e, (q, z, s) in enumerate(experts):
+        lo, hi = int(off[e]), int(off[e + 1])
+        if hi > lo:
+            y[lo:hi] = gemm(x[r_tok[lo:hi]], q, z, s, group=group, cols=cols, threads=threads)
     return y
 
 

@@ -12,6 +12,8 @@ Entry points mirror include/quick.h:
 * ``unpack_weights(packed, scales, zeros, K, N, group=128)``
 * ``w4a16_gemm(x, packed, scales, zeros, N, y=None, group=128, ...)``
 * ``select_config(M, N, K)``, ``workspace_bytes(M, N, K, cfg=None)``
+* ``grouped_gemm(x, offsets, packed, scales, zeros, N, rows=None, ...)``
+  (include/quick_grouped.h), ``pack_experts(experts)``
 """
 from __future__ import annotations
 
@@ -105,6 +107,15 @@ def lib():
             L.quick_tune_table_clear.restype = None
             L.quick_ablation_gemm.argtypes = [P, P, P, P, P, I64, I64, I64, I, P]
             L.quick_ablation_gemm.restype = I
+            L.quick_w4a16_grouped_gemm.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, P]
+            L.quick_w4a16_grouped_gemm.restype = I
+            L.quick_w4a16_grouped_gemm_ex.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, P,
+                                                      ctypes.POINTER(QuickConfig), P, SZ]
+            L.quick_w4a16_grouped_gemm_ex.restype = I
+            L.quick_grouped_workspace_bytes.argtypes = [I64, I64, I64, I64, ctypes.POINTER(QuickConfig)]
+            L.quick_grouped_workspace_bytes.restype = SZ
+            L.quick_grouped_select_config.argtypes = [I64, I64, I64, I64, ctypes.POINTER(QuickConfig)]
+            L.quick_grouped_select_config.restype = I
             _lib = L
     return _lib
 
@@ -254,6 +265,68 @@ def ablation_gemm(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, z
     return y
 
 
+def pack_experts(experts, group: int = 128):
+    """Pack E experts' (q, z, s_bits) and concatenate them into the back-to-back
+    buffers quick_w4a16_grouped_gemm takes.  Returns (packed, scales, zeros) numpy."""
+    parts = [pack_weights(q, z, s, group) for q, z, s in experts]
+    return tuple(np.concatenate([p[i] for p in parts]) for i in range(3))
+
+
+def grouped_select_config(R: int, E: int, N: int, K: int) -> dict:
+    c = QuickConfig()
+    _check(lib().quick_grouped_select_config(R, E, N, K, ctypes.byref(c)), "quick_grouped_select_config")
+    return c.as_dict()
+
+
+def grouped_workspace_bytes(R: int, E: int, N: int, K: int, cfg: QuickConfig | None = None) -> int:
+    return int(lib().quick_grouped_workspace_bytes(R, E, N, K, ctypes.byref(cfg) if cfg is not None else None))
+
+
+def grouped_gemm(x: torch.Tensor, offsets: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor,
+                 zeros: torch.Tensor, N: int, rows: torch.Tensor | None = None, R: int | None = None,
+                 y: torch.Tensor | None = None, group: int = 128, cfg: QuickConfig | None = None,
+                 workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """Grouped (mixture-of-experts) GEMM, quick_w4a16_grouped_gemm:
+    y[r] = x[rows[r]] . W_e for offsets[e] <= r < offsets[e+1].
+
+    x: [T][K] float16; offsets: int32 [E+1] on the device; rows: int32 [R] on
+    the device, or None (row r reads x[r]; R defaults to T); packed / scales /
+    zeros: the experts' buffers back to back (``pack_experts`` + ``to_device``)."""
+    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
+        raise QuickError(QUICK_ERR_INVALID_ARG, "grouped_gemm: x must be a contiguous [T][K] float16 tensor")
+    for t, name in ((offsets, "offsets"), (rows, "rows")):
+        if t is not None and (t.dtype != torch.int32 or t.dim() != 1 or not t.is_contiguous()):
+            raise QuickError(QUICK_ERR_INVALID_ARG, "grouped_gemm: %s must be a contiguous int32 vector" % name)
+    T, K = x.shape
+    E = offsets.numel() - 1
+    if rows is not None:
+        if R is not None and R != rows.numel():
+            raise QuickError(QUICK_ERR_SHAPE, "grouped_gemm: R disagrees with rows")
+        R = rows.numel()
+    elif R is None:
+        R = T
+    if y is None:
+        y = torch.empty((R, N), dtype=torch.float16, device=x.device)
+    elif y.dtype != torch.float16 or tuple(y.shape) != (R, N) or not y.is_contiguous():
+        raise QuickError(QUICK_ERR_INVALID_ARG, "grouped_gemm: y must be a contiguous [R][N] float16 tensor")
+    wb, zb, sb = packed_sizes(K, N, group)
+    for t, nb, name in ((packed, wb, "packed"), (scales, sb, "scales"), (zeros, zb, "zeros")):
+        if not t.is_contiguous() or t.numel() * t.element_size() < nb * max(E, 0):
+            raise QuickError(QUICK_ERR_SHAPE, "grouped_gemm: %s buffer too small or not contiguous" % name)
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    hs = ctypes.c_void_p(st.cuda_stream)
+    args = (_dptr(x), _dptr(rows), _dptr(offsets), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y),
+            T, R, E, N, K, group, hs)
+    if cfg is None and workspace is None:
+        rc = lib().quick_w4a16_grouped_gemm(*args)
+    else:
+        wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+        rc = lib().quick_w4a16_grouped_gemm_ex(*args, ctypes.byref(cfg) if cfg is not None else None,
+                                               _dptr(workspace), wsb)
+    _check(rc, "quick_w4a16_grouped_gemm")
+    return y
+
+
 def tune_table_save(path: str) -> None:
     _check(lib().quick_tune_table_save(os.fsencode(path)), "quick_tune_table_save")
 
@@ -275,4 +348,6 @@ EXPORTED = (
     "quick_unpack_weights", "quick_w4a16_gemm", "quick_w4a16_gemm_ex", "quick_workspace_bytes",
     "quick_select_config", "quick_tune", "quick_tune_table_save", "quick_tune_table_load",
     "quick_tune_table_size", "quick_tune_table_clear", "quick_ablation_gemm",
+    "quick_w4a16_grouped_gemm", "quick_w4a16_grouped_gemm_ex", "quick_grouped_workspace_bytes",
+    "quick_grouped_select_config",
 )

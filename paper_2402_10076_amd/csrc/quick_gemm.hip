@@ -38,6 +38,7 @@
 
 #include "quick.h"
 #include "quick_ablation.h"
+#include "quick_grouped.h"
 #include "quick_internal.h"
 
 namespace {
@@ -435,17 +436,31 @@ constexpr size_t kSkCounterBytes = QUICK_WORKSPACE_COUNTER_BYTES;
 static_assert(kSkCounterBytes >= kSkMaxWorkgroups * sizeof(unsigned), "one counter per workgroup");
 constexpr int kCoherentAux = 0x11;  // sc0 sc1: coherent across XCDs, write-through
 
+// Grouped (mixture-of-experts) form: E experts' packed weights back to back,
+// routed row r of the output multiplies token rows[r] of x (row r when rows
+// is null) with the weights of the expert e whose range
+// [offsets[e], offsets[e+1]) holds r.  The per-expert row counts live only
+// in device memory: each workgroup derives the tile list from them.
+constexpr int kMaxExperts = QUICK_MAX_EXPERTS;
+struct GroupArgs {
+    const int* rows;     // [routed] token row of each routed row, or null
+    const int* offsets;  // [experts + 1] first routed row of each expert
+    int experts;
+    int routed;          // rows of y
+};
+
 // WB != 0 builds the write-back ablation of the conventional design (the
 // dequantized weights go through an LDS tile and are read back as matrix
 // fragments): 1 = rows padded by 16 bytes (conflict-free), 2 = unpadded
 // [n][k] rows (same-bank fragment accesses).  Only the ablation library
 // launches it; WB = 0 is the method's direct-to-register path.
-template <int BM, int WN, int WB = 0>
+// GRP builds the grouped form (M is then the number of token rows of x).
+template <int BM, int WN, int WB = 0, bool GRP = false>
 __global__ void __launch_bounds__(64 * kTiledWaves, 1)
 tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
              const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
              uint16_t* __restrict__ y, float* __restrict__ ws, int M, int N, int K,
-             int kg_per_split, int n_mtiles, int n_ntiles, int n_splits)
+             int kg_per_split, int n_mtiles, int n_ntiles, int n_splits, GroupArgs ga)
 {
     constexpr int WAVES = kTiledWaves;
     constexpr int NST = kTiledStages;
@@ -482,9 +497,10 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     const int c = lane & 15;
     const int g = lane >> 4;
 
-    const rsrc_t rw = make_rsrc(pw, (uint32_t)((size_t)K * N / 2));
-    const rsrc_t rs = make_rsrc(ps, (uint32_t)((size_t)K * N / 64));
-    const rsrc_t rz = make_rsrc(pz, (uint32_t)((size_t)K * N / 256));
+    const size_t wbytes = (size_t)K * N / 2;   // packed weights of one expert
+    rsrc_t rw = make_rsrc(pw, (uint32_t)wbytes);
+    rsrc_t rs = make_rsrc(ps, (uint32_t)(wbytes / 32));
+    rsrc_t rz = make_rsrc(pz, (uint32_t)(wbytes / 128));
     const rsrc_t rx = make_rsrc(x, (uint32_t)((size_t)M * K * 2));
     const uint32_t vw = lane * 16;
     const uint32_t vs = c * 2;
@@ -492,13 +508,72 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     // this wave's DMA instruction count (wave-uniform)
     const int ndma = NDMA >= WAVES ? DMA_PER_WAVE : (wave < NDMA ? 1 : 0);
 
+    // ---- grouped form: per expert its routed rows [g_lo, g_hi) and the
+    // number of BM-row tiles of all experts before it (g_cum).  Offsets are
+    // clamped into [0, routed] so that any input stays in bounds.
+    constexpr int GE = GRP ? kMaxExperts + 1 : 1;
+    __shared__ int g_lo[GE], g_hi[GE], g_cum[GE];
+    int n_mt = n_mtiles;  // m-tiles of the tile space
+    if constexpr (GRP) {
+        if (wave == 0) {
+            int carry = 0;
+            for (int e0 = 0; e0 < ga.experts; e0 += 64) {
+                const int e = e0 + lane;
+                int lo = 0, hi = 0;
+                if (e < ga.experts) {
+                    lo = min(max(ga.offsets[e], 0), ga.routed);
+                    hi = min(max(ga.offsets[e + 1], lo), ga.routed);
+                }
+                int t = (hi - lo + BM - 1) / BM;
+#pragma unroll
+                for (int d = 1; d < 64; d <<= 1) {
+                    const int v = __shfl_up(t, d, 64);
+                    if (lane >= d) t += v;
+                }
+                if (e < ga.experts) {
+                    g_lo[e] = lo;
+                    g_hi[e] = hi;
+                    g_cum[e + 1] = carry + t;
+                }
+                carry += __shfl(t, 63, 64);
+            }
+            if (lane == 0) g_cum[0] = 0;
+        }
+        __syncthreads();
+        n_mt = uniform(g_cum[ga.experts]);
+    }
+
     // ---- per-tile state
     int m0 = 0;      // first row of the tile
+    int mend = M;    // end of the tile's rows (exclusive)
     int ntw = 0;     // first n-tile of this wave
     uint32_t ubase[NP];
     uint32_t vx[DMA_PER_WAVE];
-    auto set_tile = [&](int mtile, int ntile) __attribute__((always_inline)) {
-        m0 = mtile * BM;
+    // tile t of the tile space: M-fastest (grouped: expert, then n-tile, then
+    // the expert's m-tiles)
+    auto set_tile = [&](int t) __attribute__((always_inline)) {
+        int ntile;
+        if constexpr (GRP) {
+            // the expert whose tiles hold t: the last e with g_cum[e] * n_ntiles <= t
+            int lo = 0, hi = ga.experts;
+            while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (g_cum[mid] * n_ntiles <= t) lo = mid;
+                else hi = mid;
+            }
+            const int e = uniform(lo);
+            const int local = t - g_cum[e] * n_ntiles;
+            const int tiles_e = g_cum[e + 1] - g_cum[e];
+            ntile = local / tiles_e;
+            m0 = uniform(g_lo[e]) + (local - ntile * tiles_e) * BM;
+            mend = uniform(g_hi[e]);
+            rw = make_rsrc(pw + (size_t)e * (wbytes / 16), (uint32_t)wbytes);
+            rs = make_rsrc(ps + (size_t)e * (wbytes / 64), (uint32_t)(wbytes / 32));
+            rz = make_rsrc(pz + (size_t)e * (wbytes / 512), (uint32_t)(wbytes / 128));
+        } else {
+            m0 = (t % n_mtiles) * BM;
+            ntile = (t / n_mtiles) % n_ntiles;
+        }
         // weight units of this wave's n-tiles (clamped; out-of-range tiles
         // are computed on valid data and never stored)
         ntw = ntile * (WAVES * NP) + wave * NP;
@@ -510,8 +585,13 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 #pragma unroll
         for (int i = 0; i < DMA_PER_WAVE; ++i) {
             const int rr = (wave + i * WAVES) * 4 + (lane >> 4);
-            const int row = min(m0 + rr, M - 1);
-            vx[i] = (uint32_t)(row * K + 8 * ((lane & 15) ^ (rr & 15))) * 2;
+            int row = min(m0 + rr, mend - 1);
+            if constexpr (GRP) {
+                // gather: the token row of this routed row
+                if (ga.rows) row = ga.rows[row];
+                row = min(max(row, 0), M - 1);
+            }
+            vx[i] = ((uint32_t)row * (uint32_t)K + 8 * ((lane & 15) ^ (rr & 15))) * 2;
         }
     };
 
@@ -656,26 +736,31 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 #pragma unroll
             for (int mt = 0; mt < MTT; ++mt) {
                 const int m = m0 + mt * 16 + c;
-                if (m < M) store_h4(y + (size_t)m * N + n, v[p][mt]);
+                if (m < mend) store_h4(y + (size_t)m * N + n, v[p][mt]);
             }
         }
     };
 
     if (n_splits > 0) {
         // ---- data-parallel / split-K: one (tile, K slice) per workgroup
+        // (grouped: n_mtiles is the host's upper bound of the m-tiles; the
+        // workgroups past the actual tile count exit)
         const int nblk = n_mtiles * n_ntiles * n_splits;
         const int per_xcd = gridDim.x >> 3;
         const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
         if (t >= nblk) return;
         const int split = t / (n_mtiles * n_ntiles);
-        set_tile(t % n_mtiles, (t / n_mtiles) % n_ntiles);
+        const int tin = t - split * (n_mtiles * n_ntiles);
+        if (tin >= n_mt * n_ntiles) return;
+        set_tile(tin);
         const int kb = split * kg_per_split;
         run(kb, min(KG, kb + kg_per_split));
         if (n_splits == 1) {
             store_y(acc);
             return;
         }
-        float* part = ws + kSkCounterBytes / sizeof(float) + (size_t)split * M * N;
+        const int rows_out = GRP ? ga.routed : M;
+        float* part = ws + kSkCounterBytes / sizeof(float) + (size_t)split * rows_out * N;
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
             if (ntw + p >= NT) continue;
@@ -683,7 +768,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 #pragma unroll
             for (int mt = 0; mt < MTT; ++mt) {
                 const int m = m0 + mt * 16 + c;
-                if (m < M) *reinterpret_cast<f4_t*>(part + (size_t)m * N + n) = acc[p][mt];
+                if (m < mend) *reinterpret_cast<f4_t*>(part + (size_t)m * N + n) = acc[p][mt];
             }
         }
         return;
@@ -692,15 +777,34 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     // ---- stream-K: this workgroup owns units [u0, u1) of tiles x k-groups
     // (the host launches 8 <= gridDim.x <= tiles * KG, a multiple of 8, so
     // every range is non-empty and a tile's contributors are consecutive)
-    const int G = gridDim.x;
-    const int wid = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
-    const int64_t U = (int64_t)n_mtiles * n_ntiles * KG;
-    const int64_t u0 = (int64_t)wid * U / G;
-    const int64_t u1 = (int64_t)(wid + 1) * U / G;
+    const int64_t U = (int64_t)n_mt * n_ntiles * KG;
+    int G = gridDim.x;
+    int wid = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+    int64_t u0, u1;
+    if constexpr (GRP) {
+        // the unit count is known only here: use the largest multiple of 8
+        // workgroups not above it (the rest exit), or, with fewer than 8
+        // units, one workgroup per whole tile
+        const int ge = (int)(min<int64_t>(G, U) / 8 * 8);
+        if (ge >= 8) {
+            if ((int)(blockIdx.x >> 3) >= (ge >> 3)) return;
+            G = ge;
+            wid = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+            u0 = (int64_t)wid * U / G;
+            u1 = (int64_t)(wid + 1) * U / G;
+        } else {
+            if ((int64_t)blockIdx.x * KG >= U) return;
+            u0 = (int64_t)blockIdx.x * KG;
+            u1 = u0 + KG;
+        }
+    } else {
+        u0 = (int64_t)wid * U / G;
+        u1 = (int64_t)(wid + 1) * U / G;
+    }
     unsigned* counters = reinterpret_cast<unsigned*>(ws);
     // partial-tile slot: thread-major f4 at ((wave * NP + p) * MTT + mt) * 64 + lane
     constexpr uint32_t SLOT_BYTES = (uint32_t)WAVES * NP * MTT * 64 * 16;
-    const rsrc_t rp = make_rsrc(ws + kSkCounterBytes / sizeof(float), (uint32_t)(2 * G) * SLOT_BYTES);
+    const rsrc_t rp = make_rsrc(ws + kSkCounterBytes / sizeof(float), (uint32_t)(2 * gridDim.x) * SLOT_BYTES);
     auto slot_off = [&](int p, int mt) -> uint32_t {
         return (uint32_t)((((wave * NP + p) * MTT + mt) * 64 + lane) * 16);
     };
@@ -709,7 +813,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         const int tt = (int)(u / KG);
         const int kb = (int)(u - (int64_t)tt * KG);
         const int ke = (int)min<int64_t>(KG, kb + (u1 - u));
-        set_tile(tt % n_mtiles, tt / n_mtiles);
+        set_tile(tt);
         run(kb, ke);
         if (kb == 0 && ke == KG) {
             store_y(acc);
@@ -1126,36 +1230,58 @@ int launch_stream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint1
     }
 }
 
-template <int BM, int WN>
+// nm: m-tiles of the tile space (grouped: the host's upper bound, the
+// kernel derives the actual count from the expert offsets)
+template <int BM, int WN, bool GRP>
 void launch_tiled_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
-                    const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st)
+                    const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
+                    const GroupArgs& ga)
 {
-    const int nm = ceil_div(M, BM);
+    const int nm = GRP ? (int)(((int64_t)ga.routed + (int64_t)ga.experts * (BM - 1)) / BM) : ceil_div(M, BM);
     const int nn = ceil_div(N, kTiledWaves * WN);
     if (pl.variant == kVariantStreamK) {
-        hipLaunchKernelGGL((tiled_kernel<BM, WN>), dim3(pl.split), dim3(64 * kTiledWaves), 0, st, x, pw, ps, pz,
-                           y, ws, M, N, K, 0, nm, nn, 0);
+        hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP>), dim3(pl.split), dim3(64 * kTiledWaves), 0, st, x, pw,
+                           ps, pz, y, ws, M, N, K, 0, nm, nn, 0, ga);
         return;
     }
     const int nblk = nm * nn * pl.split;
     const int grid = ceil_div(nblk, 8) * 8;
-    hipLaunchKernelGGL((tiled_kernel<BM, WN>), dim3(grid), dim3(64 * kTiledWaves), 0, st, x, pw, ps, pz, y,
-                       ws, M, N, K, pl.kgps, nm, nn, pl.split);
+    hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP>), dim3(grid), dim3(64 * kTiledWaves), 0, st, x, pw, ps, pz,
+                       y, ws, M, N, K, pl.kgps, nm, nn, pl.split, ga);
 }
 
-int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
-                 const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st)
+// Tile shapes of the grouped form.
+bool grouped_tile_supported(int bm, int wn)
 {
-    if (pl.bm == 16 && pl.wn == 32) launch_tiled_t<16, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
-    else if (pl.bm == 32 && pl.wn == 32) launch_tiled_t<32, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
-    else if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
-    else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
-    else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
-    else if (pl.bm == 128 && pl.wn == 32) launch_tiled_t<128, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
-    else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64>(pl, x, pw, ps, pz, y, ws, M, N, K, st);
-    else return QUICK_ERR_INVALID_ARG;
+    return (bm == 16 && wn == 16) || (bm == 32 && wn == 16) || (bm == 64 && wn == 32) || (bm == 128 && wn == 32);
+}
+
+// ga == nullptr: the plain GEMM; otherwise the grouped form (M = token rows).
+int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
+                 const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
+                 const GroupArgs* ga = nullptr)
+{
+    if (ga) {
+        if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga);
+        else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga);
+        else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga);
+        else if (pl.bm == 128 && pl.wn == 32)
+            launch_tiled_t<128, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga);
+        else return QUICK_ERR_INVALID_ARG;
+    } else {
+        const GroupArgs none{nullptr, nullptr, 0, 0};
+        if (pl.bm == 16 && pl.wn == 32) launch_tiled_t<16, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
+        else if (pl.bm == 32 && pl.wn == 32) launch_tiled_t<32, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
+        else if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
+        else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
+        else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
+        else if (pl.bm == 128 && pl.wn == 32)
+            launch_tiled_t<128, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
+        else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
+        else return QUICK_ERR_INVALID_ARG;
+    }
     if (pl.variant == kVariantTiled && pl.split > 1) {
-        const int64_t MN = (int64_t)M * N;
+        const int64_t MN = (int64_t)(ga ? ga->routed : M) * N;
         const int64_t MN4 = MN / 4;
         hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((MN4 + 255) / 256)), dim3(256), 0, st,
                            ws + kSkCounterBytes / sizeof(float), y, MN4, MN, pl.split);
@@ -1420,11 +1546,173 @@ extern "C" int quick_ablation_gemm(const void* x, const void* packed, const void
         hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * kTiledWaves), 0, (hipStream_t)stream,
                            static_cast<const uint16_t*>(x), static_cast<const u4_t*>(packed),
                            static_cast<const uint16_t*>(scales), static_cast<const uint32_t*>(zeros),
-                           static_cast<uint16_t*>(y), (float*)nullptr, (int)M, (int)N, (int)K, KG, nm, nn, 1);
+                           static_cast<uint16_t*>(y), (float*)nullptr, (int)M, (int)N, (int)K, KG, nm, nn, 1,
+                           GroupArgs{nullptr, nullptr, 0, 0});
     };
     (void)hipGetLastError();
     if (mode == 0) args(tiled_kernel<64, 32, 0>);
     else if (mode == 1) args(tiled_kernel<64, 32, 1>);
     else args(tiled_kernel<64, 32, 2>);
     return hipGetLastError() == hipSuccess ? QUICK_OK : QUICK_ERR_HIP;
+}
+
+// ---------------------------------------------------------------------------
+// Grouped (mixture-of-experts) GEMM: declared in quick_grouped.h.
+// ---------------------------------------------------------------------------
+namespace {
+
+int validate_grouped(const void* x, const int32_t* rows, const int32_t* offsets, const void* packed,
+                     const void* scales, const void* zeros, void* y, int64_t T, int64_t R, int64_t E, int64_t N,
+                     int64_t K, int64_t group)
+{
+    if (group != quick::kGroup) return QUICK_ERR_UNSUPPORTED;
+    if (T < 0 || R < 0 || E < 1 || E > kMaxExperts || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0)
+        return QUICK_ERR_SHAPE;
+    // 32-bit offsets inside the kernel, as for the plain GEMM (per expert)
+    if (K * N / 2 >= ((int64_t)1 << 32) || T * K >= ((int64_t)1 << 31) || R * N >= ((int64_t)1 << 31) ||
+        R > (1 << 24) || T > (1 << 24))
+        return QUICK_ERR_SHAPE;
+    if (R == 0) return QUICK_OK;
+    if (T == 0 || (!rows && T < R)) return QUICK_ERR_SHAPE;
+    if (!x || !offsets || !packed || !scales || !zeros || !y) return QUICK_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(packed, 16) || !aligned(scales, 2) || !aligned(zeros, 4) || !aligned(y, 8) ||
+        !aligned(offsets, 4) || (rows && !aligned(rows, 4)))
+        return QUICK_ERR_ALIGNMENT;
+    return QUICK_OK;
+}
+
+// Tile and schedule for R routed rows over E experts.  Rows per expert are
+// known only on the device, so the tile is chosen for the mean (R / E) and
+// the default schedule is stream-K, which spreads whatever tile count the
+// kernel finds evenly over the resident workgroups.
+int grouped_plan(int64_t R, int64_t E, int64_t N, int64_t K, const quick_config_t* cfg, Plan* pl)
+{
+    (void)N;
+    const int64_t KG = K / 128;
+    const int64_t avg = std::max<int64_t>(1, (R + E - 1) / E);
+    pl->variant = kVariantStreamK;
+    pl->split = 0;
+    pl->kgps = 0;
+    if (avg <= 16) {
+        pl->bm = 16;
+        pl->wn = 16;
+    } else if (avg <= 32) {
+        pl->bm = 32;
+        pl->wn = 16;
+    } else if (avg <= 96) {
+        pl->bm = 64;
+        pl->wn = 32;
+    } else {
+        pl->bm = 128;
+        pl->wn = 32;
+    }
+    if (cfg) {
+        if (cfg->variant < 0 || cfg->variant == kVariantStream || cfg->variant > 3 || cfg->split_k < 0)
+            return QUICK_ERR_INVALID_ARG;
+        if (cfg->variant == kVariantTiled) {
+            if (cfg->split_k > KG) return QUICK_ERR_INVALID_ARG;
+            pl->variant = kVariantTiled;
+            pl->split = cfg->split_k ? cfg->split_k : 1;
+        } else if (cfg->split_k) {
+            if (cfg->split_k % 8 != 0 || cfg->split_k > kSkMaxWorkgroups) return QUICK_ERR_INVALID_ARG;
+            pl->split = cfg->split_k;
+        }
+        if (cfg->tile_m) pl->bm = cfg->tile_m;
+        if (cfg->tile_n) pl->wn = cfg->tile_n;
+        if (!grouped_tile_supported(pl->bm, pl->wn)) return QUICK_ERR_INVALID_ARG;
+    }
+    if (pl->variant == kVariantStreamK) {
+        const int g = pl->split ? pl->split : tiled_resident(pl->bm, pl->wn);
+        pl->split = std::max(8, std::min(g, kSkMaxWorkgroups) / 8 * 8);
+    } else {
+        pl->kgps = ceil_div(KG, pl->split);
+        pl->split = ceil_div(KG, pl->kgps);  // no empty splits
+    }
+    return QUICK_OK;
+}
+
+size_t grouped_workspace(int64_t R, int64_t N, const Plan& pl)
+{
+    if (pl.variant == kVariantTiled && pl.split > 1)
+        return kSkCounterBytes + (size_t)pl.split * R * N * sizeof(float);
+    if (pl.variant == kVariantStreamK) return kSkCounterBytes + 2 * (size_t)pl.split * sk_slot_bytes(pl.bm, pl.wn);
+    return 0;
+}
+
+int grouped_impl(const void* x, const int32_t* rows, const int32_t* offsets, const void* packed,
+                 const void* scales, const void* zeros, void* y, int64_t T, int64_t R, int64_t E, int64_t N,
+                 int64_t K, int64_t group, void* stream, const quick_config_t* cfg, void* workspace,
+                 size_t workspace_bytes)
+{
+    int st = validate_grouped(x, rows, offsets, packed, scales, zeros, y, T, R, E, N, K, group);
+    if (st) return st;
+    Plan pl;
+    st = grouped_plan(R, E, N, K, cfg, &pl);
+    if (st) return st;
+    if (R == 0) return QUICK_OK;
+    hipStream_t hs = (hipStream_t)stream;
+    const size_t need = grouped_workspace(R, N, pl);
+    void* ws = nullptr;
+    if (need) {
+        if (workspace) {
+            if (workspace_bytes < need) return QUICK_ERR_WORKSPACE;
+            if (!aligned(workspace, 16)) return QUICK_ERR_ALIGNMENT;
+            ws = workspace;
+        } else {
+            st = get_workspace(need, hs, &ws);
+            if (st) return st;
+        }
+    }
+    const GroupArgs ga{rows, offsets, (int)E, (int)R};
+    (void)hipGetLastError();
+    st = launch_tiled(pl, static_cast<const uint16_t*>(x), static_cast<const u4_t*>(packed),
+                      static_cast<const uint16_t*>(scales), static_cast<const uint32_t*>(zeros),
+                      static_cast<uint16_t*>(y), static_cast<float*>(ws), (int)T, (int)N, (int)K, hs, &ga);
+    if (st) return st;
+    return hipGetLastError() == hipSuccess ? QUICK_OK : QUICK_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" int quick_w4a16_grouped_gemm(const void* x, const int32_t* rows, const int32_t* offsets,
+                                        const void* packed, const void* scales, const void* zeros, void* y,
+                                        int64_t T, int64_t R, int64_t E, int64_t N, int64_t K, int64_t group,
+                                        void* stream)
+{
+    return grouped_impl(x, rows, offsets, packed, scales, zeros, y, T, R, E, N, K, group, stream, nullptr,
+                        nullptr, 0);
+}
+
+extern "C" int quick_w4a16_grouped_gemm_ex(const void* x, const int32_t* rows, const int32_t* offsets,
+                                           const void* packed, const void* scales, const void* zeros, void* y,
+                                           int64_t T, int64_t R, int64_t E, int64_t N, int64_t K, int64_t group,
+                                           void* stream, const quick_config_t* cfg, void* workspace,
+                                           size_t workspace_bytes)
+{
+    return grouped_impl(x, rows, offsets, packed, scales, zeros, y, T, R, E, N, K, group, stream, cfg, workspace,
+                        workspace_bytes);
+}
+
+extern "C" size_t quick_grouped_workspace_bytes(int64_t R, int64_t E, int64_t N, int64_t K,
+                                                const quick_config_t* cfg)
+{
+    if (R <= 0 || E < 1 || E > kMaxExperts || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return 0;
+    Plan pl;
+    if (grouped_plan(R, E, N, K, cfg, &pl)) return 0;
+    return grouped_workspace(R, N, pl);
+}
+
+extern "C" int quick_grouped_select_config(int64_t R, int64_t E, int64_t N, int64_t K, quick_config_t* cfg)
+{
+    if (!cfg) return QUICK_ERR_INVALID_ARG;
+    if (R < 0 || E < 1 || E > kMaxExperts || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0)
+        return QUICK_ERR_SHAPE;
+    Plan pl;
+    const int st = grouped_plan(R, E, N, K, nullptr, &pl);
+    if (st) return st;
+    cfg->variant = pl.variant;
+    cfg->split_k = pl.split;
+    cfg->tile_m = pl.bm;
+    cfg->tile_n = pl.wn;
+    return QUICK_OK;
 }

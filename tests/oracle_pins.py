@@ -139,6 +139,36 @@ def pin_exact_fraction():
                 assert abs(y[m, n] - float(tot)) <= bound, "exact brute force mismatch at (%d,%d)" % (m, n)
 
 
+def pin_grouped_exact_fraction():
+    """The mixture-of-experts form on a tiny case, by exact rational
+    arithmetic written out per routed row: 3 experts (one owning no rows),
+    gathered token rows with repeats and out of order."""
+    g = _rng(410)
+    T, K, N = 5, 128, 16
+    x = _f16(g.standard_normal((T, K)))
+    experts = []
+    for e in range(3):
+        experts.append((g.integers(0, 16, (K, N), dtype=np.uint8), g.integers(0, 16, (1, N), dtype=np.uint8),
+                        _f16(g.uniform(0.002, 0.02, (1, N)))))
+    offsets = [0, 3, 3, 7]               # expert 1 owns no rows
+    rows = [4, 0, 4, 2, 1, 3, 0]
+    y = oracle.grouped_gemm(x, rows, offsets, experts)
+    assert y.shape == (7, N)
+    xf = [[Fraction(float(v)) for v in r] for r in x.view(np.float16)]
+    for r in range(7):
+        e = 0 if r < 3 else 2
+        q, z, s = experts[e]
+        for n in range(N):
+            sf = Fraction(float(s.view(np.float16)[0, n]))
+            tot = Fraction(0)
+            mag = Fraction(0)
+            for k in range(K):
+                t = xf[rows[r]][k] * (int(q[k, n]) - int(z[0, n])) * sf
+                tot += t
+                mag += abs(t)
+            assert abs(y[r, n] - float(tot)) <= float(mag) * K * 2.0 ** -52, "grouped mismatch at (%d,%d)" % (r, n)
+
+
 def pin_zero_when_z_equals_q():
     M, K, N = 3, 256, 32
     g = _rng(400)
@@ -246,6 +276,7 @@ ALL_PINS = [
     pin_integer_case,
     pin_closed_form,
     pin_exact_fraction,
+    pin_grouped_exact_fraction,
     pin_zero_when_z_equals_q,
     pin_scale_doubling,
     pin_dequant_is_identity_gemm,

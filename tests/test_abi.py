@@ -38,6 +38,7 @@ def test_header_is_plain_c_and_links():
     prog = r'''
 #include "quick.h"
 #include "quick_ablation.h"
+#include "quick_grouped.h"
 #include <stdio.h>
 #include <string.h>
 int main(void) {
@@ -51,6 +52,8 @@ int main(void) {
     if (quick_select_config(1, 4096, 4096, &cfg) != QUICK_OK || cfg.variant != 1) return 5;
     if (quick_w4a16_gemm(0, 0, 0, 0, 0, 0, 4096, 4096, 128, 0) != QUICK_OK) return 6;
     if (quick_ablation_gemm(0, 0, 0, 0, 0, 4, 4096, 4096, 3, 0) != QUICK_ERR_INVALID_ARG) return 7;
+    if (quick_w4a16_grouped_gemm(0, 0, 0, 0, 0, 0, 0, 16, 0, 8, 4096, 4096, 128, 0) != QUICK_OK) return 8;
+    if (QUICK_MAX_EXPERTS != 512) return 9;
     printf("%s\n", quick_status_string(QUICK_ERR_SHAPE));
     return 0;
 }
@@ -124,6 +127,57 @@ def test_gemm_ex_validation_without_device():
     assert Q.workspace_bytes(256, 4096, 4096, sk) == Q.WS_COUNTER_BYTES + 2 * 1024 * 128 * 256 * 4
     # fewer than 8 units: one workgroup per tile, no workspace
     assert Q.workspace_bytes(16, 128, 512, Q.make_config(variant=3, tile_m=16, tile_n=16)) == 0
+
+
+def test_grouped_validation_without_device():
+    """Every argument check of the grouped entry point returns before any
+    device work."""
+    A = 0x10000
+    L = Q.lib()
+
+    def g(x=A, rows=A, offs=A, pw=A, ps=A, pz=A, y=A, T=64, R=128, E=8, N=4096, K=4096, group=128, cfg=None):
+        if cfg is None:
+            return L.quick_w4a16_grouped_gemm(x, rows, offs, pw, ps, pz, y, T, R, E, N, K, group, None)
+        return L.quick_w4a16_grouped_gemm_ex(x, rows, offs, pw, ps, pz, y, T, R, E, N, K, group, None,
+                                             ctypes.byref(cfg), None, 0)
+    assert g(R=0) == Q.QUICK_OK
+    assert g(0, 0, 0, 0, 0, 0, 0, R=0) == Q.QUICK_OK
+    assert g(group=64) == Q.QUICK_ERR_UNSUPPORTED
+    assert g(E=0) == Q.QUICK_ERR_SHAPE
+    assert g(E=513) == Q.QUICK_ERR_SHAPE
+    assert g(R=-1) == Q.QUICK_ERR_SHAPE
+    assert g(T=-1) == Q.QUICK_ERR_SHAPE
+    assert g(K=4000) == Q.QUICK_ERR_SHAPE
+    assert g(N=4088) == Q.QUICK_ERR_SHAPE
+    assert g(T=0) == Q.QUICK_ERR_SHAPE              # routed rows need token rows
+    assert g(rows=0, T=64, R=128) == Q.QUICK_ERR_SHAPE   # identity rows need T >= R
+    assert g(N=1 << 20, K=1 << 17) == Q.QUICK_ERR_SHAPE
+    assert g(x=0) == Q.QUICK_ERR_INVALID_ARG
+    assert g(offs=0) == Q.QUICK_ERR_INVALID_ARG
+    assert g(y=0) == Q.QUICK_ERR_INVALID_ARG
+    assert g(x=A + 8) == Q.QUICK_ERR_ALIGNMENT
+    assert g(offs=A + 2) == Q.QUICK_ERR_ALIGNMENT
+    assert g(rows=A + 2) == Q.QUICK_ERR_ALIGNMENT
+    assert g(y=A + 4) == Q.QUICK_ERR_ALIGNMENT
+    assert g(cfg=Q.make_config(variant=1)) == Q.QUICK_ERR_INVALID_ARG      # no stream kernel here
+    assert g(cfg=Q.make_config(variant=4)) == Q.QUICK_ERR_INVALID_ARG
+    assert g(cfg=Q.make_config(variant=2, tile_m=16, tile_n=32)) == Q.QUICK_ERR_INVALID_ARG
+    assert g(cfg=Q.make_config(variant=2, split_k=33)) == Q.QUICK_ERR_INVALID_ARG
+    assert g(cfg=Q.make_config(variant=3, split_k=12)) == Q.QUICK_ERR_INVALID_ARG
+    # workspaces: split-K partials over all routed rows; stream-K slots per workgroup
+    cfg = Q.make_config(variant=2, split_k=4, tile_m=64, tile_n=32)
+    assert Q.grouped_workspace_bytes(1024, 8, 14336, 4096, cfg) == Q.WS_COUNTER_BYTES + 4 * 1024 * 14336 * 4
+    cfg = Q.make_config(variant=3, split_k=64, tile_m=128, tile_n=32)
+    assert Q.grouped_workspace_bytes(1024, 8, 14336, 4096, cfg) == Q.WS_COUNTER_BYTES + 2 * 64 * 128 * 256 * 4
+    assert Q.grouped_workspace_bytes(1024, 8, 14336, 4096, Q.make_config(variant=2, tile_m=16, tile_n=16)) == 0
+    assert Q.grouped_workspace_bytes(0, 8, 14336, 4096) == 0
+
+
+def test_grouped_select_config():
+    assert Q.grouped_select_config(1024, 8, 14336, 4096)["tile_m"] == 128   # ~128 rows per expert
+    assert Q.grouped_select_config(64, 8, 14336, 4096)["tile_m"] == 16      # decode-sized batches
+    c = Q.grouped_select_config(1024, 8, 4096, 14336)
+    assert c["variant"] == Q.VARIANT_STREAMK and c["split_k"] % 8 == 0
 
 
 def test_select_config_regimes():

@@ -9,6 +9,7 @@ import pytest
 import torch
 
 import oracle
+import paper_2402_10076_amd as Q
 import workloads as W
 from gpu_util import TOL, Packed, from_dev_y, rel_err, say, to_dev_x
 
@@ -50,3 +51,37 @@ def test_mixtral_experts():
             q, z, s = W.mixtral_expert_weights(e, which)
             x = xt[routes[e]] if which < 2 else W.mixtral_w2_input(e, Me)
             _check_point("C4 expert%d %s" % (e, name), Packed(q, z, s), x, q, z, s, Me)
+
+
+def test_mixtral_grouped():
+    """The same expert GEMMs as one grouped launch per weight (w1, w3 over
+    the routed tokens, gathered in the kernel; w2 over the experts' stacked
+    inputs), each expert's block against the oracle on sampled outputs."""
+    routes = W.mixtral_routing()
+    xt = W.mixtral_tokens()
+    counts = [len(r) for r in routes]
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    rows = np.concatenate(routes).astype(np.int32)
+    od = torch.from_numpy(offsets).cuda()
+    rd = torch.from_numpy(rows).cuda()
+    for which, name in enumerate(("w1", "w3", "w2")):
+        experts = [W.mixtral_expert_weights(e, which) for e in range(W.MIXTRAL_EXPERTS)]
+        K, N = experts[0][0].shape
+        dw, ds, dz = Q.to_device(*Q.pack_experts(experts))
+        if which < 2:
+            x = xt
+            y = from_dev_y(Q.grouped_gemm(to_dev_x(xt), od, dw, ds, dz, N, rows=rd))
+        else:
+            x = np.concatenate([W.mixtral_w2_input(e, counts[e]) for e in range(W.MIXTRAL_EXPERTS)])
+            y = from_dev_y(Q.grouped_gemm(to_dev_x(x), od, dw, ds, dz, N))
+        cols = W.sample_columns(N, 256)
+        for e in range(W.MIXTRAL_EXPERTS):
+            lo = offsets[e]
+            sub = W.sample_rows(counts[e])
+            xr = x[rows[lo + sub]] if which < 2 else x[lo + sub]
+            ref = oracle.gemm(xr, *experts[e], cols=cols)
+            err = rel_err(y[np.ix_(lo + sub, cols)], ref)
+            say("C4 grouped %s expert%d M=%d rel_err=%.3g" % (name, e, counts[e], err))
+            assert err <= TOL
+        del dw, ds, dz
+        torch.cuda.empty_cache()
