@@ -112,12 +112,19 @@ int quick_w4a16_gemm(const void* x, const void* packed, const void* scales,
 typedef struct quick_config {
     int variant;   /* 0 auto, 1 = stream kernel (small M), 2 = tiled kernel,
                       3 = tiled kernel with the stream-K schedule (resident
-                      workgroups share the tiles x k-groups work equally)     */
+                      workgroups share the tiles x k-groups work equally),
+                      4 = balanced stream kernel (M <= 16, M*K*2 bytes
+                      <= 128 KiB and K a multiple of 2048: every wave of the
+                      chip streams an equal share of the 16 x 128 weight
+                      units)                                                 */
     int split_k;   /* variant 2: K slices across workgroups; variant 1: waves
                       per workgroup (1, 2, 4, 8); variant 3: resident
                       workgroups, a multiple of 8 up to 4096 (clamped to the
-                      number of tile x 128-channel units); 0 = auto          */
-    int tile_m;    /* tiled kernel rows per workgroup: 16, 32, 64 or 128;
+                      number of tile x 128-channel units); variant 4:
+                      workgroups of 8 waves, up to 512 (0 = one per compute
+                      unit); 0 = auto                                        */
+    int tile_m;    /* tiled kernel rows per workgroup: 16, 32, 64 or 128
+                      (variant 4: must be 0, as tile_n);
                       supported (tile_m, tile_n) pairs: (16|32, 16|32),
                       (64, 32), (64, 64), (128, 32)                         */
     int tile_n;    /* tiled kernel columns per wave: 16, 32 or 64
