@@ -11,6 +11,8 @@ The arithmetic lives in ``oracle.c`` (plain C, binary64):
 * ``gemm``     -- y = x . W as a naive loop over k in ascending order.
 * ``grouped_gemm`` (Python) -- the mixture-of-experts form: each expert's
   rows are ``gemm`` of its gathered token rows.
+* ``epilogue`` / ``interleave_gate_up`` (Python) -- the fused output
+  epilogue (bias, gated SiLU) and the gate/up column order it reads.
 * ``pack``     -- the QPK16 offline reorder written as its element-wise
   definition (paper, Section 3.2 describes reordering the static weights
   offline to the matrix-instruction operand pattern and to the dequantizer's
@@ -196,6 +198,31 @@ def grouped_gemm(x_bits, rows, offsets, experts, group: int = 128, cols=None, th
         if hi > lo:
             y[lo:hi] = gemm(x[r_tok[lo:hi]], q, z, s, group=group, cols=cols, threads=threads)
     return y
+
+
+def epilogue(h, bias_bits=None, act: int = 0) -> np.ndarray:
+    """Output epilogue of the fused GEMM in binary64: h + bias (bias as
+    binary16 bits), then for act = 1 the gated SiLU of alternating 16-column
+    gate / up tiles, y[m][16t + i] = silu(h[m][32t + i]) * h[m][32t + 16 + i],
+    silu(a) = a / (1 + exp(-a))."""
+    h = np.asarray(h, np.float64)
+    if bias_bits is not None:
+        h = h + f16_to_f64(bias_bits)[None, :]
+    if act == 0:
+        return h
+    M, N = h.shape
+    tiles = h.reshape(M, N // 32, 2, 16)
+    gate, up = tiles[:, :, 0, :], tiles[:, :, 1, :]
+    return (gate / (1.0 + np.exp(-gate)) * up).reshape(M, N // 2)
+
+
+def interleave_gate_up(gate, up) -> np.ndarray:
+    """Columns of two [R][Nh] arrays alternated in 16-column tiles: output
+    column 32t + i is gate column 16t + i (i < 16), else up column 16t + i - 16."""
+    g = np.asarray(gate)
+    u = np.asarray(up)
+    R, Nh = g.shape
+    return np.stack([g.reshape(R, Nh // 16, 16), u.reshape(R, Nh // 16, 16)], axis=2).reshape(R, 2 * Nh)
 
 
 def pack(q, z, s_bits, group: int = 128):

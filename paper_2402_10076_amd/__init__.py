@@ -14,6 +14,8 @@ Entry points mirror include/quick.h:
 * ``select_config(M, N, K)``, ``workspace_bytes(M, N, K, cfg=None)``
 * ``grouped_gemm(x, offsets, packed, scales, zeros, N, rows=None, ...)``
   (include/quick_grouped.h), ``pack_experts(experts)``
+* ``gemm_fused`` / ``grouped_gemm_fused`` with a bias and the gated SiLU
+  (include/quick_fused.h), ``interleave_gate_up(gate, up)``
 """
 from __future__ import annotations
 
@@ -64,6 +66,14 @@ class QuickConfig(ctypes.Structure):
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+class QuickEpilogue(ctypes.Structure):
+    _fields_ = [("bias", ctypes.c_void_p), ("activation", ctypes.c_int)]
+
+
+ACT_NONE = 0
+ACT_SILU_GATE = 1
 
 
 def lib():
@@ -117,6 +127,19 @@ def lib():
             L.quick_grouped_workspace_bytes.restype = SZ
             L.quick_grouped_select_config.argtypes = [I64, I64, I64, I64, ctypes.POINTER(QuickConfig)]
             L.quick_grouped_select_config.restype = I
+            EP = ctypes.POINTER(QuickEpilogue)
+            L.quick_w4a16_gemm_fused.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P, EP,
+                                                 ctypes.POINTER(QuickConfig), P, SZ]
+            L.quick_w4a16_gemm_fused.restype = I
+            L.quick_w4a16_grouped_gemm_fused.argtypes = [P, P, P, P, P, P, P, I64, I64, I64, I64, I64, I64, P, EP,
+                                                         ctypes.POINTER(QuickConfig), P, SZ]
+            L.quick_w4a16_grouped_gemm_fused.restype = I
+            L.quick_fused_workspace_bytes.argtypes = [I64, I64, I64, ctypes.POINTER(QuickConfig), EP]
+            L.quick_fused_workspace_bytes.restype = SZ
+            L.quick_grouped_fused_workspace_bytes.argtypes = [I64, I64, I64, I64, ctypes.POINTER(QuickConfig), EP]
+            L.quick_grouped_fused_workspace_bytes.restype = SZ
+            L.quick_interleave_gate_up.argtypes = [P, P, P, P, P, P, I64, I64, I64, P, P, P]
+            L.quick_interleave_gate_up.restype = I
             _lib = L
     return _lib
 
@@ -328,6 +351,84 @@ def grouped_gemm(x: torch.Tensor, offsets: torch.Tensor, packed: torch.Tensor, s
     return y
 
 
+def interleave_gate_up(gate, up, group: int = 128):
+    """quick_interleave_gate_up: the column order the gated epilogue expects,
+    from unpacked (q, z, s_bits) of the gate and up matrices ([K][Nh] each)."""
+    qg, zg, sg = (np.ascontiguousarray(a) for a in gate)
+    qu, zu, su = (np.ascontiguousarray(a) for a in up)
+    K, Nh = qg.shape
+    q = np.empty((K, 2 * Nh), np.uint8)
+    z = np.empty((K // group, 2 * Nh), np.uint8)
+    s = np.empty((K // group, 2 * Nh), np.uint16)
+    _check(lib().quick_interleave_gate_up(_np_ptr(qg.astype(np.uint8)), _np_ptr(zg.astype(np.uint8)),
+                                          _np_ptr(sg.astype(np.uint16)), _np_ptr(qu.astype(np.uint8)),
+                                          _np_ptr(zu.astype(np.uint8)), _np_ptr(su.astype(np.uint16)),
+                                          K, Nh, group, _np_ptr(q), _np_ptr(z), _np_ptr(s)),
+           "quick_interleave_gate_up")
+    return q, z, s
+
+
+def _epi(bias, activation):
+    return QuickEpilogue(ctypes.c_void_p(bias.data_ptr()) if bias is not None else None, int(activation))
+
+
+def fused_workspace_bytes(M, N, K, cfg=None, bias=None, activation=0) -> int:
+    e = _epi(bias, activation)
+    return int(lib().quick_fused_workspace_bytes(M, N, K, ctypes.byref(cfg) if cfg is not None else None,
+                                                 ctypes.byref(e)))
+
+
+def gemm_fused(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor, N: int,
+               bias: torch.Tensor | None = None, activation: int = ACT_NONE, y: torch.Tensor | None = None,
+               group: int = 128, cfg: QuickConfig | None = None, workspace: torch.Tensor | None = None,
+               stream=None) -> torch.Tensor:
+    """quick_w4a16_gemm_fused: y = epilogue(x . W + bias); ``activation`` =
+    ACT_SILU_GATE gives the [M][N/2] gated SiLU of interleaved gate/up tiles."""
+    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
+        raise QuickError(QUICK_ERR_INVALID_ARG, "gemm_fused: x must be a contiguous [M][K] float16 tensor")
+    if bias is not None and (bias.dtype != torch.float16 or not bias.is_contiguous()):
+        raise QuickError(QUICK_ERR_INVALID_ARG, "gemm_fused: bias must be a contiguous float16 tensor")
+    M, K = x.shape
+    n_out = N // 2 if activation == ACT_SILU_GATE else N
+    if y is None:
+        y = torch.empty((M, n_out), dtype=torch.float16, device=x.device)
+    elif y.dtype != torch.float16 or tuple(y.shape) != (M, n_out) or not y.is_contiguous():
+        raise QuickError(QUICK_ERR_INVALID_ARG, "gemm_fused: y must be a contiguous [M][%d] float16 tensor" % n_out)
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    e = _epi(bias, activation)
+    wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().quick_w4a16_gemm_fused(_dptr(x), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y), M, N, K,
+                                        group, ctypes.c_void_p(st.cuda_stream), ctypes.byref(e),
+                                        ctypes.byref(cfg) if cfg is not None else None, _dptr(workspace), wsb),
+           "quick_w4a16_gemm_fused")
+    return y
+
+
+def grouped_gemm_fused(x: torch.Tensor, offsets: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor,
+                       zeros: torch.Tensor, N: int, rows: torch.Tensor | None = None, R: int | None = None,
+                       bias: torch.Tensor | None = None, activation: int = ACT_NONE,
+                       y: torch.Tensor | None = None, group: int = 128, cfg: QuickConfig | None = None,
+                       workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    """quick_w4a16_grouped_gemm_fused: the grouped GEMM with the epilogue
+    (bias [E][N] per expert)."""
+    T, K = x.shape
+    E = offsets.numel() - 1
+    R = rows.numel() if rows is not None else (T if R is None else R)
+    n_out = N // 2 if activation == ACT_SILU_GATE else N
+    if y is None:
+        y = torch.empty((R, n_out), dtype=torch.float16, device=x.device)
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    e = _epi(bias, activation)
+    wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().quick_w4a16_grouped_gemm_fused(_dptr(x), _dptr(rows), _dptr(offsets), _dptr(packed),
+                                                _dptr(scales), _dptr(zeros), _dptr(y), T, R, E, N, K, group,
+                                                ctypes.c_void_p(st.cuda_stream), ctypes.byref(e),
+                                                ctypes.byref(cfg) if cfg is not None else None,
+                                                _dptr(workspace), wsb),
+           "quick_w4a16_grouped_gemm_fused")
+    return y
+
+
 def tune_table_save(path: str) -> None:
     _check(lib().quick_tune_table_save(os.fsencode(path)), "quick_tune_table_save")
 
@@ -350,5 +451,6 @@ EXPORTED = (
     "quick_select_config", "quick_tune", "quick_tune_table_save", "quick_tune_table_load",
     "quick_tune_table_size", "quick_tune_table_clear", "quick_ablation_gemm",
     "quick_w4a16_grouped_gemm", "quick_w4a16_grouped_gemm_ex", "quick_grouped_workspace_bytes",
-    "quick_grouped_select_config",
+    "quick_grouped_select_config", "quick_w4a16_gemm_fused", "quick_w4a16_grouped_gemm_fused",
+    "quick_fused_workspace_bytes", "quick_grouped_fused_workspace_bytes", "quick_interleave_gate_up",
 )

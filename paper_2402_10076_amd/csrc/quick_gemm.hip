@@ -38,6 +38,7 @@
 
 #include "quick.h"
 #include "quick_ablation.h"
+#include "quick_fused.h"
 #include "quick_grouped.h"
 #include "quick_internal.h"
 
@@ -135,6 +136,53 @@ __device__ __forceinline__ void store_h4(uint16_t* dst, const f4_t& v)
     *reinterpret_cast<u2_t*>(dst) = o;
 }
 
+// Output epilogue applied to the fp32 accumulators before the single
+// rounding to f16: an optional per-column bias, then either nothing or the
+// gated SiLU of a fused gate/up projection whose packed columns alternate
+// in 16-column tiles (gate tile t at packed columns 32t .. 32t+15, the
+// matching up tile at 32t+16 .. 32t+31):
+//   y[m][16t + i] = silu(h[m][32t + i]) * h[m][32t + 16 + i],
+//   silu(a) = a / (1 + e^-a),  h = x . W (+ bias).
+struct Epi {
+    const uint16_t* bias;  // f16 [N] in packed column order, or null
+    int act;               // 0 none, 1 gated SiLU (output has N/2 columns)
+};
+
+__device__ __forceinline__ f4_t add_bias(f4_t v, const uint16_t* bias, int n)
+{
+    if (bias) {
+        const u2_t b = *reinterpret_cast<const u2_t*>(bias + n);
+        v[0] += (float)bits_as<_Float16>((uint16_t)(b[0] & 0xFFFFu));
+        v[1] += (float)bits_as<_Float16>((uint16_t)(b[0] >> 16));
+        v[2] += (float)bits_as<_Float16>((uint16_t)(b[1] & 0xFFFFu));
+        v[3] += (float)bits_as<_Float16>((uint16_t)(b[1] >> 16));
+    }
+    return v;
+}
+
+__device__ __forceinline__ f4_t silu_gate(const f4_t& a, const f4_t& b)
+{
+    f4_t r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) r[i] = a[i] / (1.f + __expf(-a[i])) * b[i];
+    return r;
+}
+
+// Store 4 consecutive packed columns n .. n+3 of row m (act == 0), or, for
+// the gated form, the gate quad at n (n % 32 < 16) with its up quad `u` at
+// n + 16 as output columns n/32*16 + n%32 .. +3; N = packed columns.
+__device__ __forceinline__ void store_out(uint16_t* y, const Epi& e, int64_t m, int N, int n, f4_t v)
+{
+    v = add_bias(v, e.bias, n);
+    store_h4(y + m * N + n, v);
+}
+__device__ __forceinline__ void store_gated(uint16_t* y, const Epi& e, int64_t m, int N, int n, f4_t gate, f4_t up)
+{
+    gate = add_bias(gate, e.bias, n);
+    up = add_bias(up, e.bias, n + 16);
+    store_h4(y + m * (N / 2) + (n >> 5) * 16 + (n & 15), silu_gate(gate, up));
+}
+
 // Raw buffer loads: a wave-uniform 128-bit descriptor (base, byte size) in
 // SGPRs, a per-lane byte offset in a VGPR and a wave-uniform byte offset in an
 // SGPR, so per-iteration address arithmetic is scalar.  Offsets at or beyond
@@ -217,7 +265,7 @@ template <int MT, int NPW, int WAVES, int D, bool XL>
 __global__ void __launch_bounds__(64 * WAVES)
 stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
               const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
-              uint16_t* __restrict__ y, int M, int N, int K)
+              uint16_t* __restrict__ y, int M, int N, int K, Epi epi)
 {
     static_assert(D % 2 == 0, "ring depth must be even (activation double buffer parity)");
     extern __shared__ __attribute__((aligned(16))) uint8_t xlds[];
@@ -364,14 +412,20 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         }
     }
 
+    // (gated form: NPW == 2 and nt0 even, so acc[0] / acc[1] are a gate
+    // tile and its up tile)
     if constexpr (WAVES == 1) {
 #pragma unroll
-        for (int p = 0; p < NPW; ++p) {
-            if (nt0 + p >= NT) continue;
-            const int n = (nt0 + p) * 16 + 4 * g;
+        for (int mt = 0; mt < MT; ++mt) {
+            const int m = mt * 16 + c;
+            if (m >= M) continue;
+            if (NPW == 2 && epi.act) {
+                if (nt0 < NT) store_gated(y, epi, m, N, nt0 * 16 + 4 * g, acc[0][mt], acc[NPW - 1][mt]);
+                continue;
+            }
 #pragma unroll
-            for (int mt = 0; mt < MT; ++mt)
-                if (mt * 16 + c < M) store_h4(y + (size_t)(mt * 16 + c) * N + n, acc[p][mt]);
+            for (int p = 0; p < NPW; ++p)
+                if (nt0 + p < NT) store_out(y, epi, m, N, (nt0 + p) * 16 + 4 * g, acc[p][mt]);
         }
     } else {
         __shared__ f4_t red[WAVES][NPW * MT][64];
@@ -380,17 +434,30 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 #pragma unroll
             for (int mt = 0; mt < MT; ++mt) red[wave][p * MT + mt][lane] = acc[p][mt];
         __syncthreads();
-        for (int item = threadIdx.x; item < NPW * MT * 64; item += 64 * WAVES) {
-            const int l = item & 63;
-            const int pm = item >> 6;
-            const int p = pm / MT;
-            const int mt = pm % MT;
-            const int m = mt * 16 + (l & 15);
-            if (nt0 + p >= NT || m >= M) continue;
+        auto total = [&](int pm, int l) {
             f4_t sum = red[0][pm][l];
 #pragma unroll
             for (int w = 1; w < WAVES; ++w) sum += red[w][pm][l];
-            store_h4(y + (size_t)m * N + (nt0 + p) * 16 + 4 * (l >> 4), sum);
+            return sum;
+        };
+        if (NPW == 2 && epi.act) {
+            for (int item = threadIdx.x; item < MT * 64; item += 64 * WAVES) {
+                const int l = item & 63;
+                const int mt = item >> 6;
+                const int m = mt * 16 + (l & 15);
+                if (nt0 >= NT || m >= M) continue;
+                store_gated(y, epi, m, N, nt0 * 16 + 4 * (l >> 4), total(mt, l), total((NPW - 1) * MT + mt, l));
+            }
+        } else {
+            for (int item = threadIdx.x; item < NPW * MT * 64; item += 64 * WAVES) {
+                const int l = item & 63;
+                const int pm = item >> 6;
+                const int p = pm / MT;
+                const int mt = pm % MT;
+                const int m = mt * 16 + (l & 15);
+                if (nt0 + p >= NT || m >= M) continue;
+                store_out(y, epi, m, N, (nt0 + p) * 16 + 4 * (l >> 4), total(pm, l));
+            }
         }
     }
 }
@@ -474,7 +541,7 @@ __global__ void __launch_bounds__(64 * kTiledWaves, 1)
 tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
              const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
              uint16_t* __restrict__ y, float* __restrict__ ws, int M, int N, int K,
-             int kg_per_split, int n_mtiles, int n_ntiles, int n_splits, GroupArgs ga)
+             int kg_per_split, int n_mtiles, int n_ntiles, int n_splits, GroupArgs ga, Epi epi)
 {
     constexpr int WAVES = kTiledWaves;
     constexpr int NST = kTiledStages;
@@ -557,6 +624,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         n_mt = uniform(g_cum[ga.experts]);
     }
 
+    const uint16_t* const bias0 = epi.bias;
     // ---- per-tile state
     int m0 = 0;      // first row of the tile
     int mend = M;    // end of the tile's rows (exclusive)
@@ -581,6 +649,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
             ntile = local / tiles_e;
             m0 = uniform(g_lo[e]) + (local - ntile * tiles_e) * BM;
             mend = uniform(g_hi[e]);
+            if (bias0) epi.bias = bias0 + (size_t)e * N;   // bias [E][N]
             rw = make_rsrc(pw + (size_t)e * (wbytes / 16), (uint32_t)wbytes);
             rs = make_rsrc(ps + (size_t)e * (wbytes / 64), (uint32_t)(wbytes / 32));
             rz = make_rsrc(pz + (size_t)e * (wbytes / 512), (uint32_t)(wbytes / 128));
@@ -742,7 +811,21 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         }
     };
 
+    // (gated form: NP even and ntw even, so tiles p, p+1 are a gate tile
+    // and its up tile)
     auto store_y = [&](const f4_t (&v)[NP][MTT]) __attribute__((always_inline)) {
+        if (NP % 2 == 0 && epi.act) {
+#pragma unroll
+            for (int p = 0; p < NP; p += 2) {
+                if (ntw + p >= NT) continue;
+#pragma unroll
+                for (int mt = 0; mt < MTT; ++mt) {
+                    const int m = m0 + mt * 16 + c;
+                    if (m < mend) store_gated(y, epi, m, N, (ntw + p) * 16 + 4 * g, v[p][mt], v[(p + 1) % NP][mt]);
+                }
+            }
+            return;
+        }
 #pragma unroll
         for (int p = 0; p < NP; ++p) {
             if (ntw + p >= NT) continue;
@@ -750,7 +833,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 #pragma unroll
             for (int mt = 0; mt < MTT; ++mt) {
                 const int m = m0 + mt * 16 + c;
-                if (m < mend) store_h4(y + (size_t)m * N + n, v[p][mt]);
+                if (m < mend) store_out(y, epi, m, N, n, v[p][mt]);
             }
         }
     };
@@ -1107,17 +1190,29 @@ bstream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     }
 }
 
-// Sum of S fp32 partial outputs in split order, rounded once to f16.
+// Sum of S fp32 partial outputs [S][rows][N] in split order, then the
+// epilogue and one rounding to f16.  One thread per 4 output columns.
 __global__ void __launch_bounds__(256)
-splitk_reduce_kernel(const float* __restrict__ ws, uint16_t* __restrict__ y, int64_t MN4, int64_t MN,
-                     int S)
+splitk_reduce_kernel(const float* __restrict__ ws, uint16_t* __restrict__ y, int64_t rows, int N, int S, Epi epi)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= MN4) return;
-    const f4_t* p = reinterpret_cast<const f4_t*>(ws) + i;
-    f4_t sum = p[0];
-    for (int s = 1; s < S; ++s) sum += p[(size_t)s * (MN / 4)];
-    store_h4(y + i * 4, sum);
+    const int quads = (epi.act ? N / 2 : N) / 4;   // output quads per row
+    if (i >= rows * quads) return;
+    const int64_t m = i / quads;
+    const int q = (int)(i - m * quads);
+    const int64_t plane = rows * N / 4;             // quads per split
+    auto sum_at = [&](int n) {
+        const f4_t* p = reinterpret_cast<const f4_t*>(ws) + (m * N + n) / 4;
+        f4_t sum = p[0];
+        for (int s = 1; s < S; ++s) sum += p[(size_t)s * plane];
+        return sum;
+    };
+    if (epi.act) {
+        const int n = (q >> 2) * 32 + (q & 3) * 4;   // gate quad; its up quad is 16 columns on
+        store_gated(y, epi, m, N, n, sum_at(n), sum_at(n + 16));
+    } else {
+        store_out(y, epi, m, N, q * 4, sum_at(q * 4));
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -1462,7 +1557,7 @@ int get_workspace(size_t need, hipStream_t stream, void** out)
 
 template <int MT, int NPW, int WAVES>
 void launch_stream_t(const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz,
-                     uint16_t* y, int M, int N, int K, hipStream_t st)
+                     uint16_t* y, int M, int N, int K, hipStream_t st, const Epi& epi)
 {
     const int NT = N / 16;
     dim3 grid((NT + NPW - 1) / NPW);
@@ -1471,23 +1566,23 @@ void launch_stream_t(const uint16_t* x, const u4_t* pw, const uint16_t* ps, cons
     if (MT == 1 && xbytes <= kStreamLdsX) {
         constexpr int D = NPW == 1 ? 16 : 8;
         hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D, true>), grid, dim3(64 * WAVES), xbytes, st,
-                           x, pw, ps, pz, y, M, N, K);
+                           x, pw, ps, pz, y, M, N, K, epi);
     } else {
         constexpr int D = MT == 1 ? (NPW == 1 ? 8 : 4) : 2;
         hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D, false>), grid, dim3(64 * WAVES), 0, st, x, pw, ps,
-                           pz, y, M, N, K);
+                           pz, y, M, N, K, epi);
     }
 }
 
 template <int MT, int NPW>
 int launch_stream_w(int waves, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
-                    const uint32_t* pz, uint16_t* y, int M, int N, int K, hipStream_t st)
+                    const uint32_t* pz, uint16_t* y, int M, int N, int K, hipStream_t st, const Epi& epi)
 {
     switch (waves) {
-    case 1: launch_stream_t<MT, NPW, 1>(x, pw, ps, pz, y, M, N, K, st); break;
-    case 2: launch_stream_t<MT, NPW, 2>(x, pw, ps, pz, y, M, N, K, st); break;
-    case 4: launch_stream_t<MT, NPW, 4>(x, pw, ps, pz, y, M, N, K, st); break;
-    case 8: launch_stream_t<MT, NPW, 8>(x, pw, ps, pz, y, M, N, K, st); break;
+    case 1: launch_stream_t<MT, NPW, 1>(x, pw, ps, pz, y, M, N, K, st, epi); break;
+    case 2: launch_stream_t<MT, NPW, 2>(x, pw, ps, pz, y, M, N, K, st, epi); break;
+    case 4: launch_stream_t<MT, NPW, 4>(x, pw, ps, pz, y, M, N, K, st, epi); break;
+    case 8: launch_stream_t<MT, NPW, 8>(x, pw, ps, pz, y, M, N, K, st, epi); break;
     default: return QUICK_ERR_INVALID_ARG;
     }
     return QUICK_OK;
@@ -1495,22 +1590,22 @@ int launch_stream_w(int waves, const uint16_t* x, const u4_t* pw, const uint16_t
 
 template <int MT>
 int launch_stream_n(int npw, int waves, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
-                    const uint32_t* pz, uint16_t* y, int M, int N, int K, hipStream_t st)
+                    const uint32_t* pz, uint16_t* y, int M, int N, int K, hipStream_t st, const Epi& epi)
 {
-    if (npw == 1) return launch_stream_w<MT, 1>(waves, x, pw, ps, pz, y, M, N, K, st);
-    if (npw == 2) return launch_stream_w<MT, 2>(waves, x, pw, ps, pz, y, M, N, K, st);
+    if (npw == 1) return launch_stream_w<MT, 1>(waves, x, pw, ps, pz, y, M, N, K, st, epi);
+    if (npw == 2) return launch_stream_w<MT, 2>(waves, x, pw, ps, pz, y, M, N, K, st, epi);
     return QUICK_ERR_INVALID_ARG;
 }
 
 int launch_stream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
-                  const uint32_t* pz, uint16_t* y, int M, int N, int K, hipStream_t st)
+                  const uint32_t* pz, uint16_t* y, int M, int N, int K, hipStream_t st, const Epi& epi)
 {
     const int mt = (M + 15) / 16;
     switch (mt) {
-    case 1: return launch_stream_n<1>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st);
-    case 2: return launch_stream_n<2>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st);
-    case 3: return launch_stream_n<3>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st);
-    case 4: return launch_stream_n<4>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st);
+    case 1: return launch_stream_n<1>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st, epi);
+    case 2: return launch_stream_n<2>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st, epi);
+    case 3: return launch_stream_n<3>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st, epi);
+    case 4: return launch_stream_n<4>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st, epi);
     default: return QUICK_ERR_INVALID_ARG;
     }
 }
@@ -1520,56 +1615,58 @@ int launch_stream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint1
 template <int BM, int WN, bool GRP>
 void launch_tiled_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
                     const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
-                    const GroupArgs& ga)
+                    const GroupArgs& ga, const Epi& epi)
 {
     const int nm = GRP ? (int)(((int64_t)ga.routed + (int64_t)ga.experts * (BM - 1)) / BM) : ceil_div(M, BM);
     const int nn = ceil_div(N, kTiledWaves * WN);
     if (pl.variant == kVariantStreamK) {
         hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP>), dim3(pl.split), dim3(64 * kTiledWaves), 0, st, x, pw,
-                           ps, pz, y, ws, M, N, K, 0, nm, nn, 0, ga);
+                           ps, pz, y, ws, M, N, K, 0, nm, nn, 0, ga, epi);
         return;
     }
     const int nblk = nm * nn * pl.split;
     const int grid = ceil_div(nblk, 8) * 8;
     hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP>), dim3(grid), dim3(64 * kTiledWaves), 0, st, x, pw, ps, pz,
-                       y, ws, M, N, K, pl.kgps, nm, nn, pl.split, ga);
+                       y, ws, M, N, K, pl.kgps, nm, nn, pl.split, ga, epi);
 }
 
 // Tile shapes of the grouped form.
 bool grouped_tile_supported(int bm, int wn)
 {
-    return (bm == 16 && wn == 16) || (bm == 32 && wn == 16) || (bm == 64 && wn == 32) || (bm == 128 && wn == 32);
+    return ((bm == 16 || bm == 32) && (wn == 16 || wn == 32)) || (bm == 64 && wn == 32) || (bm == 128 && wn == 32);
 }
 
 // ga == nullptr: the plain GEMM; otherwise the grouped form (M = token rows).
 int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
                  const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
-                 const GroupArgs* ga = nullptr)
+                 const Epi& epi, const GroupArgs* ga = nullptr)
 {
     if (ga) {
-        if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga);
-        else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga);
-        else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga);
+        if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
+        else if (pl.bm == 16 && pl.wn == 32) launch_tiled_t<16, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
+        else if (pl.bm == 32 && pl.wn == 32) launch_tiled_t<32, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
+        else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
+        else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
         else if (pl.bm == 128 && pl.wn == 32)
-            launch_tiled_t<128, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga);
+            launch_tiled_t<128, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
         else return QUICK_ERR_INVALID_ARG;
     } else {
         const GroupArgs none{nullptr, nullptr, 0, 0};
-        if (pl.bm == 16 && pl.wn == 32) launch_tiled_t<16, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
-        else if (pl.bm == 32 && pl.wn == 32) launch_tiled_t<32, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
-        else if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
-        else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
-        else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
+        if (pl.bm == 16 && pl.wn == 32) launch_tiled_t<16, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 32 && pl.wn == 32) launch_tiled_t<32, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
         else if (pl.bm == 128 && pl.wn == 32)
-            launch_tiled_t<128, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
-        else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none);
+            launch_tiled_t<128, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
         else return QUICK_ERR_INVALID_ARG;
     }
     if (pl.variant == kVariantTiled && pl.split > 1) {
-        const int64_t MN = (int64_t)(ga ? ga->routed : M) * N;
-        const int64_t MN4 = MN / 4;
-        hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((MN4 + 255) / 256)), dim3(256), 0, st,
-                           ws + kSkCounterBytes / sizeof(float), y, MN4, MN, pl.split);
+        const int64_t rows = ga ? ga->routed : M;
+        const int64_t quads = rows * (epi.act ? N / 2 : N) / 4;
+        hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, st,
+                           ws + kSkCounterBytes / sizeof(float), y, rows, N, pl.split, epi);
     }
     return QUICK_OK;
 }
@@ -1615,14 +1712,45 @@ int validate(const void* x, const void* packed, const void* scales, const void* 
     return QUICK_OK;
 }
 
+// The epilogue's constraints on a plan.  The gated form needs each gate
+// tile and its up tile in one wave (stream kernel: 2 n-tiles per wave;
+// tiled kernel: an even number of 16-column tiles per wave) unless a split-K
+// reduction pass applies it; the balanced stream kernel has no epilogue.
+// Choices left automatic are adjusted; an explicit one that conflicts (a
+// tile_n the caller set, the balanced stream kernel) is an error.
+int epilogue_plan(int64_t M, int64_t N, int64_t K, const Epi& epi, const quick_config_t* cfg, Plan* pl)
+{
+    if (!epi.bias && !epi.act) return QUICK_OK;
+    if (pl->variant == kVariantBStream) {
+        if (cfg && cfg->variant == kVariantBStream) return QUICK_ERR_INVALID_ARG;
+        auto_plan(M, N, K, pl);
+    }
+    if (!epi.act) return QUICK_OK;
+    const bool fixed_n = cfg && cfg->tile_n;
+    if (pl->variant == kVariantStream && pl->wn != 2) {
+        if (fixed_n) return QUICK_ERR_INVALID_ARG;
+        pl->wn = 2;
+    }
+    if (is_tiled(pl->variant) && pl->wn == 16 && !(pl->variant == kVariantTiled && pl->split > 1)) {
+        if (fixed_n || pl->bm > 32) return QUICK_ERR_INVALID_ARG;
+        pl->wn = 32;
+    }
+    return QUICK_OK;
+}
+
 int gemm_impl(const void* x, const void* packed, const void* scales, const void* zeros, void* y,
               int64_t M, int64_t N, int64_t K, int64_t group, void* stream, const quick_config_t* cfg,
-              void* workspace, size_t workspace_bytes)
+              void* workspace, size_t workspace_bytes, const Epi& epi = Epi{nullptr, 0})
 {
     int st = validate(x, packed, scales, zeros, y, M, N, K, group);
     if (st) return st;
+    if (epi.act < 0 || epi.act > 1) return QUICK_ERR_INVALID_ARG;
+    if (epi.act && N % 32 != 0) return QUICK_ERR_SHAPE;
+    if (M && epi.bias && !aligned(epi.bias, 8)) return QUICK_ERR_ALIGNMENT;
     Plan pl;
     st = make_plan(M, N, K, cfg, &pl);
+    if (st) return st;
+    st = epilogue_plan(M, N, K, epi, cfg, &pl);
     if (st) return st;
     if (M == 0) return QUICK_OK;
     finish_plan(M, N, K, &pl);
@@ -1646,11 +1774,11 @@ int gemm_impl(const void* x, const void* packed, const void* scales, const void*
     uint16_t* yy = static_cast<uint16_t*>(y);
     (void)hipGetLastError();  // clear a stale error so the check below is ours
     if (pl.variant == kVariantStream)
-        st = launch_stream(pl, xx, pw, ps, pz, yy, (int)M, (int)N, (int)K, hs);
+        st = launch_stream(pl, xx, pw, ps, pz, yy, (int)M, (int)N, (int)K, hs, epi);
     else if (pl.variant == kVariantBStream)
         st = launch_bstream(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs);
     else
-        st = launch_tiled(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs);
+        st = launch_tiled(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs, epi);
     if (st) return st;
     if (hipGetLastError() != hipSuccess) return QUICK_ERR_HIP;
     return QUICK_OK;
@@ -1854,7 +1982,7 @@ extern "C" int quick_ablation_gemm(const void* x, const void* packed, const void
                            static_cast<const uint16_t*>(x), static_cast<const u4_t*>(packed),
                            static_cast<const uint16_t*>(scales), static_cast<const uint32_t*>(zeros),
                            static_cast<uint16_t*>(y), (float*)nullptr, (int)M, (int)N, (int)K, KG, nm, nn, 1,
-                           GroupArgs{nullptr, nullptr, 0, 0});
+                           GroupArgs{nullptr, nullptr, 0, 0}, Epi{nullptr, 0});
     };
     (void)hipGetLastError();
     if (mode == 0) args(tiled_kernel<64, 32, 0>);
@@ -1946,15 +2074,34 @@ size_t grouped_workspace(int64_t R, int64_t N, const Plan& pl)
     return 0;
 }
 
+// The epilogue's constraints on a grouped plan (see epilogue_plan).
+int grouped_epilogue_plan(const Epi& epi, const quick_config_t* cfg, Plan* pl)
+{
+    // a per-expert bias is added in the tile epilogue; the split-K reduction
+    // pass does not know a row's expert
+    if (epi.bias && pl->variant == kVariantTiled && pl->split > 1) return QUICK_ERR_INVALID_ARG;
+    if (epi.act && pl->wn == 16 && !(pl->variant == kVariantTiled && pl->split > 1)) {
+        // 16-column waves cannot pair a gate tile with its up tile
+        if (cfg && cfg->tile_n) return QUICK_ERR_INVALID_ARG;
+        pl->wn = 32;
+    }
+    return QUICK_OK;
+}
+
 int grouped_impl(const void* x, const int32_t* rows, const int32_t* offsets, const void* packed,
                  const void* scales, const void* zeros, void* y, int64_t T, int64_t R, int64_t E, int64_t N,
                  int64_t K, int64_t group, void* stream, const quick_config_t* cfg, void* workspace,
-                 size_t workspace_bytes)
+                 size_t workspace_bytes, const Epi& epi = Epi{nullptr, 0})
 {
     int st = validate_grouped(x, rows, offsets, packed, scales, zeros, y, T, R, E, N, K, group);
     if (st) return st;
+    if (epi.act < 0 || epi.act > 1) return QUICK_ERR_INVALID_ARG;
+    if (epi.act && N % 32 != 0) return QUICK_ERR_SHAPE;
+    if (R && epi.bias && !aligned(epi.bias, 8)) return QUICK_ERR_ALIGNMENT;
     Plan pl;
     st = grouped_plan(R, E, N, K, cfg, &pl);
+    if (st) return st;
+    st = grouped_epilogue_plan(epi, cfg, &pl);
     if (st) return st;
     if (R == 0) return QUICK_OK;
     hipStream_t hs = (hipStream_t)stream;
@@ -1974,7 +2121,7 @@ int grouped_impl(const void* x, const int32_t* rows, const int32_t* offsets, con
     (void)hipGetLastError();
     st = launch_tiled(pl, static_cast<const uint16_t*>(x), static_cast<const u4_t*>(packed),
                       static_cast<const uint16_t*>(scales), static_cast<const uint32_t*>(zeros),
-                      static_cast<uint16_t*>(y), static_cast<float*>(ws), (int)T, (int)N, (int)K, hs, &ga);
+                      static_cast<uint16_t*>(y), static_cast<float*>(ws), (int)T, (int)N, (int)K, hs, epi, &ga);
     if (st) return st;
     return hipGetLastError() == hipSuccess ? QUICK_OK : QUICK_ERR_HIP;
 }
@@ -2021,5 +2168,79 @@ extern "C" int quick_grouped_select_config(int64_t R, int64_t E, int64_t N, int6
     cfg->split_k = pl.split;
     cfg->tile_m = pl.bm;
     cfg->tile_n = pl.wn;
+    return QUICK_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Fused epilogues: declared in quick_fused.h.
+// ---------------------------------------------------------------------------
+namespace {
+
+Epi to_epi(const quick_epilogue_t* e)
+{
+    return e ? Epi{static_cast<const uint16_t*>(e->bias), e->activation} : Epi{nullptr, 0};
+}
+
+}  // namespace
+
+extern "C" int quick_w4a16_gemm_fused(const void* x, const void* packed, const void* scales, const void* zeros,
+                                      void* y, int64_t M, int64_t N, int64_t K, int64_t group, void* stream,
+                                      const quick_epilogue_t* epi, const quick_config_t* cfg, void* workspace,
+                                      size_t workspace_bytes)
+{
+    return gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, cfg, workspace, workspace_bytes,
+                     to_epi(epi));
+}
+
+extern "C" int quick_w4a16_grouped_gemm_fused(const void* x, const int32_t* rows, const int32_t* offsets,
+                                              const void* packed, const void* scales, const void* zeros, void* y,
+                                              int64_t T, int64_t R, int64_t E, int64_t N, int64_t K,
+                                              int64_t group, void* stream, const quick_epilogue_t* epi,
+                                              const quick_config_t* cfg, void* workspace, size_t workspace_bytes)
+{
+    return grouped_impl(x, rows, offsets, packed, scales, zeros, y, T, R, E, N, K, group, stream, cfg, workspace,
+                        workspace_bytes, to_epi(epi));
+}
+
+extern "C" size_t quick_fused_workspace_bytes(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg,
+                                              const quick_epilogue_t* epi)
+{
+    if (M <= 0 || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return 0;
+    Plan pl;
+    if (make_plan(M, N, K, cfg, &pl)) return 0;
+    if (epilogue_plan(M, N, K, to_epi(epi), cfg, &pl)) return 0;
+    finish_plan(M, N, K, &pl);
+    return plan_workspace(M, N, pl);
+}
+
+extern "C" size_t quick_grouped_fused_workspace_bytes(int64_t R, int64_t E, int64_t N, int64_t K,
+                                                      const quick_config_t* cfg, const quick_epilogue_t* epi)
+{
+    if (R <= 0 || E < 1 || E > kMaxExperts || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return 0;
+    Plan pl;
+    if (grouped_plan(R, E, N, K, cfg, &pl)) return 0;
+    if (grouped_epilogue_plan(to_epi(epi), cfg, &pl)) return 0;
+    return grouped_workspace(R, N, pl);
+}
+
+extern "C" int quick_interleave_gate_up(const uint8_t* q_gate, const uint8_t* z_gate, const uint16_t* s_gate,
+                                        const uint8_t* q_up, const uint8_t* z_up, const uint16_t* s_up,
+                                        int64_t K, int64_t Nh, int64_t group, uint8_t* q, uint8_t* z, uint16_t* s)
+{
+    if (!q_gate || !z_gate || !s_gate || !q_up || !z_up || !s_up || !q || !z || !s) return QUICK_ERR_INVALID_ARG;
+    if (group != quick::kGroup) return QUICK_ERR_UNSUPPORTED;
+    if (K <= 0 || Nh <= 0 || K % 128 != 0 || Nh % 16 != 0) return QUICK_ERR_SHAPE;
+    const int64_t N = 2 * Nh;
+    // output column 32t + i: gate column 16t + i (i < 16), up column 16t + i - 16
+    auto cols = [&](const auto* gate, const auto* up, auto* out, int64_t rows) {
+        for (int64_t r = 0; r < rows; ++r)
+            for (int64_t t = 0; t < Nh / 16; ++t) {
+                std::memcpy(out + r * N + 32 * t, gate + r * Nh + 16 * t, 16 * sizeof(*out));
+                std::memcpy(out + r * N + 32 * t + 16, up + r * Nh + 16 * t, 16 * sizeof(*out));
+            }
+    };
+    cols(q_gate, q_up, q, K);
+    cols(z_gate, z_up, z, K / group);
+    cols(s_gate, s_up, s, K / group);
     return QUICK_OK;
 }

@@ -169,6 +169,42 @@ def pin_grouped_exact_fraction():
             assert abs(y[r, n] - float(tot)) <= float(mag) * K * 2.0 ** -52, "grouped mismatch at (%d,%d)" % (r, n)
 
 
+def pin_epilogue_invariants():
+    """The fused epilogue against facts of the mathematics: silu(a) - silu(-a)
+    = a (a*sigmoid(a) + a*sigmoid(-a) = a), silu(0) = 0, silu(a) -> a for
+    large a and -> 0 for very negative a; an up factor of 1 leaves silu
+    alone; a bias adds exactly its binary16 value; and the tile layout maps
+    gate column 32t+i and up column 32t+16+i to output 16t+i."""
+    g = _rng(420)
+    M, Nh = 3, 48
+    a = g.standard_normal((M, Nh)) * 4
+    one = np.ones((M, Nh))
+    y_pos = oracle.epilogue(oracle.interleave_gate_up(a, one), act=1)
+    y_neg = oracle.epilogue(oracle.interleave_gate_up(-a, one), act=1)
+    assert np.allclose(y_pos - y_neg, a, rtol=1e-12, atol=1e-15), "silu antisymmetry"
+    big = oracle.epilogue(oracle.interleave_gate_up(np.full((1, 16), 40.0), np.full((1, 16), 3.0)), act=1)
+    assert np.all(big == 120.0), "silu(40) * 3"
+    neg = oracle.epilogue(oracle.interleave_gate_up(np.full((1, 16), -40.0), np.full((1, 16), 3.0)), act=1)
+    assert np.all(np.abs(neg) < 1e-15) and np.all(neg < 0), "silu(-40)"
+    zero = oracle.epilogue(oracle.interleave_gate_up(np.zeros((1, 16)), np.full((1, 16), 7.0)), act=1)
+    assert np.all(zero == 0.0), "silu(0)"
+    # the layout: each output column reads its own gate and up column
+    gate = np.arange(Nh, dtype=np.float64)[None, :] * 0.01
+    up = 1.0 + np.arange(Nh, dtype=np.float64)[None, :]
+    h = oracle.interleave_gate_up(gate, up)
+    assert h[0, 0] == gate[0, 0] and h[0, 15] == gate[0, 15] and h[0, 16] == up[0, 0]
+    assert h[0, 31] == up[0, 15] and h[0, 32] == gate[0, 16] and h[0, 48] == up[0, 16]
+    y = oracle.epilogue(h, act=1)
+    want = gate / (1.0 + np.exp(-gate)) * up
+    assert np.allclose(y, want, rtol=1e-15), "gate/up pairing"
+    # bias: small integers, exact in binary16 and binary64
+    b = _f16(g.integers(-8, 9, 2 * Nh).astype(np.float64))
+    hi = g.integers(-100, 100, (M, 2 * Nh)).astype(np.float64)
+    hb = oracle.epilogue(hi, bias_bits=b)
+    assert np.array_equal(hb - hi, np.broadcast_to(b.view(np.float16).astype(np.float64), hi.shape)), "bias add"
+    assert np.array_equal(oracle.epilogue(hi, bias_bits=b, act=1), oracle.epilogue(hb, act=1))
+
+
 def pin_zero_when_z_equals_q():
     M, K, N = 3, 256, 32
     g = _rng(400)
@@ -277,6 +313,7 @@ ALL_PINS = [
     pin_closed_form,
     pin_exact_fraction,
     pin_grouped_exact_fraction,
+    pin_epilogue_invariants,
     pin_zero_when_z_equals_q,
     pin_scale_doubling,
     pin_dequant_is_identity_gemm,

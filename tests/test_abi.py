@@ -38,6 +38,7 @@ def test_header_is_plain_c_and_links():
     prog = r'''
 #include "quick.h"
 #include "quick_ablation.h"
+#include "quick_fused.h"
 #include "quick_grouped.h"
 #include <stdio.h>
 #include <string.h>
@@ -54,6 +55,8 @@ int main(void) {
     if (quick_ablation_gemm(0, 0, 0, 0, 0, 4, 4096, 4096, 3, 0) != QUICK_ERR_INVALID_ARG) return 7;
     if (quick_w4a16_grouped_gemm(0, 0, 0, 0, 0, 0, 0, 16, 0, 8, 4096, 4096, 128, 0) != QUICK_OK) return 8;
     if (QUICK_MAX_EXPERTS != 512) return 9;
+    quick_epilogue_t e = {0, QUICK_ACT_SILU_GATE};
+    if (quick_w4a16_gemm_fused(0, 0, 0, 0, 0, 0, 4096, 4096, 128, 0, &e, 0, 0, 0) != QUICK_OK) return 10;
     printf("%s\n", quick_status_string(QUICK_ERR_SHAPE));
     return 0;
 }
@@ -171,7 +174,7 @@ def test_grouped_validation_without_device():
     assert g(y=A + 4) == Q.QUICK_ERR_ALIGNMENT
     assert g(cfg=Q.make_config(variant=1)) == Q.QUICK_ERR_INVALID_ARG      # no stream kernel here
     assert g(cfg=Q.make_config(variant=4)) == Q.QUICK_ERR_INVALID_ARG
-    assert g(cfg=Q.make_config(variant=2, tile_m=16, tile_n=32)) == Q.QUICK_ERR_INVALID_ARG
+    assert g(cfg=Q.make_config(variant=2, tile_m=16, tile_n=64)) == Q.QUICK_ERR_INVALID_ARG
     assert g(cfg=Q.make_config(variant=2, split_k=33)) == Q.QUICK_ERR_INVALID_ARG
     assert g(cfg=Q.make_config(variant=3, split_k=12)) == Q.QUICK_ERR_INVALID_ARG
     # workspaces: split-K partials over all routed rows; stream-K slots per workgroup
@@ -181,6 +184,40 @@ def test_grouped_validation_without_device():
     assert Q.grouped_workspace_bytes(1024, 8, 14336, 4096, cfg) == Q.WS_COUNTER_BYTES + 2 * 64 * 128 * 256 * 4
     assert Q.grouped_workspace_bytes(1024, 8, 14336, 4096, Q.make_config(variant=2, tile_m=16, tile_n=16)) == 0
     assert Q.grouped_workspace_bytes(0, 8, 14336, 4096) == 0
+
+
+def test_fused_validation_without_device():
+    """Argument checks of the fused entry points, and the plans the gated
+    epilogue forces, before any device work."""
+    A = 0x10000
+    L = Q.lib()
+
+    def f(act=1, bias=None, M=4, N=4096, K=4096, cfg=None):
+        e = Q.QuickEpilogue(bias, act)
+        return L.quick_w4a16_gemm_fused(A, A, A, A, A, M, N, K, 128, None, ctypes.byref(e),
+                                        ctypes.byref(cfg) if cfg is not None else None, None, 0)
+    assert f(M=0) == Q.QUICK_OK
+    assert f(act=2) == Q.QUICK_ERR_INVALID_ARG
+    assert f(N=4112) == Q.QUICK_ERR_SHAPE                     # gated: N a multiple of 32
+    assert f(act=0, bias=A + 2) == Q.QUICK_ERR_ALIGNMENT
+    # explicit configurations that cannot pair gate and up tiles in a wave
+    assert f(cfg=Q.make_config(variant=1, split_k=4, tile_n=1)) == Q.QUICK_ERR_INVALID_ARG
+    assert f(cfg=Q.make_config(variant=2, split_k=1, tile_m=16, tile_n=16)) == Q.QUICK_ERR_INVALID_ARG
+    assert f(cfg=Q.make_config(variant=3, tile_m=32, tile_n=16)) == Q.QUICK_ERR_INVALID_ARG
+    assert f(cfg=Q.make_config(variant=2, tile_m=64, tile_n=16)) == Q.QUICK_ERR_INVALID_ARG
+    assert f(act=0, bias=A, cfg=Q.make_config(variant=4)) == Q.QUICK_ERR_INVALID_ARG
+    # a split-K reduction applies the epilogue itself: 16-column waves are fine;
+    # the gated output needs the same partials as the plain GEMM
+    cfg = Q.make_config(variant=2, split_k=4, tile_m=16, tile_n=16)
+    assert Q.fused_workspace_bytes(64, 4096, 4096, cfg, activation=1) == Q.workspace_bytes(64, 4096, 4096, cfg)
+    # stream-K with the automatic 16-column tile moves to 32-column waves (bigger slots)
+    sk = Q.make_config(variant=3, split_k=64, tile_m=16)
+    assert Q.fused_workspace_bytes(64, 4096, 4096, sk, activation=1) == Q.WS_COUNTER_BYTES + 2 * 64 * 16 * 256 * 4
+    # a per-expert bias cannot go through the split-K reduction
+    e = Q.QuickEpilogue(A, 0)
+    assert L.quick_w4a16_grouped_gemm_fused(A, A, A, A, A, A, A, 64, 128, 8, 4096, 4096, 128, None,
+                                            ctypes.byref(e), ctypes.byref(Q.make_config(variant=2, split_k=2)),
+                                            None, 0) == Q.QUICK_ERR_INVALID_ARG
 
 
 def test_grouped_select_config():

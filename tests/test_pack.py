@@ -84,3 +84,17 @@ def test_pack_errors_leave_outputs_untouched():
     assert Q.lib().quick_pack_weights(None, P(z), P(s), K, N, 128, P(pw), P(ps), P(pz)) == Q.QUICK_ERR_INVALID_ARG
     with pytest.raises(Q.QuickError):
         Q.pack_weights(np.full((K, N), 16, np.uint8), z, s)
+
+
+def test_interleave_gate_up_matches_oracle_layout():
+    """The library's gate/up column interleave equals the oracle's, byte for
+    byte, for q, z and s."""
+    g = np.random.Generator(np.random.PCG64(31))
+    K, Nh = 256, 48
+    gate = (g.integers(0, 16, (K, Nh), dtype=np.uint8), g.integers(0, 16, (K // 128, Nh), dtype=np.uint8),
+            g.integers(0, 1 << 15, (K // 128, Nh)).astype(np.uint16))
+    up = (g.integers(0, 16, (K, Nh), dtype=np.uint8), g.integers(0, 16, (K // 128, Nh), dtype=np.uint8),
+          g.integers(0, 1 << 15, (K // 128, Nh)).astype(np.uint16))
+    q, z, s = Q.interleave_gate_up(gate, up)
+    for got, a, b in zip((q, z, s), gate, up):
+        assert np.array_equal(got, oracle.interleave_gate_up(a, b))
