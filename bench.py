@@ -416,6 +416,27 @@ def moe(reps=20, sweep=True):
                          speedup=round(t_dense / t, 3), max_rel_diff_vs_dense=round(diff, 6)))
         log("  3 grouped launches %-40s %9.2f us  %7.1f TFLOP/s  %.2fx  (max rel diff vs dense %.2g)" % (
             name, t, flops / t / 1e6, t_dense / t, diff))
+    # the layer as it runs: w1 and w3 as one grouped launch over their
+    # interleaved columns with the gated SiLU fused into the epilogue, then
+    # w2 over that output (the SiLU-gated product never leaves registers in
+    # f32 and is rounded once)
+    q13 = []
+    for e in range(8):
+        g1 = W.mixtral_expert_weights(e, 0)
+        g3 = W.mixtral_expert_weights(e, 1)
+        q13.append(Q.interleave_gate_up(g1, g3))
+    w13 = Q.to_device(*Q.pack_experts(q13))
+    h13 = torch.empty(R, 14336, dtype=torch.float16, device="cuda")
+    y2 = torch.empty(R, 4096, dtype=torch.float16, device="cuda")
+
+    def chain():
+        Q.grouped_gemm_fused(xt, od, *w13, 2 * 14336, rows=rd, activation=Q.ACT_SILU_GATE, y=h13)
+        Q.grouped_gemm(h13, od, *mats[2]["w"], 4096, y=y2)
+
+    t = timed(chain, [h13, y2])
+    rows.append(dict(form="2 grouped launches: w1|w3 with the fused gated SiLU, then w2 on its output",
+                     us=round(t, 2), tflops=round(flops / t / 1e6, 1), speedup=round(t_dense / t, 3)))
+    log("  2 grouped launches, fused SiLU gate    %9.2f us  %7.1f TFLOP/s  %.2fx" % (t, flops / t / 1e6, t_dense / t))
     return dict(routed_rows=R, rows_per_expert=counts, gflop=round(flops / 1e9, 2), rows=rows)
 
 
