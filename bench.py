@@ -72,7 +72,7 @@ def launch_sequence(points):
         if sel["variant"] == 1:
             seq.append((p["kernel"], "stream_kernel<"))
         else:
-            seq.append((p["kernel"], "tiled_kernel<%d, %d, 0, false>" % (sel["tile_m"], sel["tile_n"])))
+            seq.append((p["kernel"], "tiled_kernel<%d, %d, 0, false, false>" % (sel["tile_m"], sel["tile_n"])))
             if sel["variant"] == 2 and sel["split_k"] > 1:
                 seq.append((None, "splitk_reduce_kernel"))
     return seq

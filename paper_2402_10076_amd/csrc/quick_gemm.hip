@@ -536,7 +536,9 @@ struct GroupArgs {
 // [n][k] rows (same-bank fragment accesses).  Only the ablation library
 // launches it; WB = 0 is the method's direct-to-register path.
 // GRP builds the grouped form (M is then the number of token rows of x).
-template <int BM, int WN, int WB = 0, bool GRP = false>
+// EP builds the output epilogue (bias, gated SiLU); without it the stores
+// are plain roundings and the kernel carries none of its code.
+template <int BM, int WN, int WB = 0, bool GRP = false, bool EP = false>
 __global__ void __launch_bounds__(64 * kTiledWaves, 1)
 tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
              const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
@@ -649,7 +651,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
             ntile = local / tiles_e;
             m0 = uniform(g_lo[e]) + (local - ntile * tiles_e) * BM;
             mend = uniform(g_hi[e]);
-            if (bias0) epi.bias = bias0 + (size_t)e * N;   // bias [E][N]
+            if (EP && bias0) epi.bias = bias0 + (size_t)e * N;   // bias [E][N]
             rw = make_rsrc(pw + (size_t)e * (wbytes / 16), (uint32_t)wbytes);
             rs = make_rsrc(ps + (size_t)e * (wbytes / 64), (uint32_t)(wbytes / 32));
             rz = make_rsrc(pz + (size_t)e * (wbytes / 512), (uint32_t)(wbytes / 128));
@@ -814,6 +816,19 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     // (gated form: NP even and ntw even, so tiles p, p+1 are a gate tile
     // and its up tile)
     auto store_y = [&](const f4_t (&v)[NP][MTT]) __attribute__((always_inline)) {
+        if constexpr (!EP) {
+#pragma unroll
+            for (int p = 0; p < NP; ++p) {
+                if (ntw + p >= NT) continue;
+                const int n = (ntw + p) * 16 + 4 * g;
+#pragma unroll
+                for (int mt = 0; mt < MTT; ++mt) {
+                    const int m = m0 + mt * 16 + c;
+                    if (m < mend) store_h4(y + (size_t)m * N + n, v[p][mt]);
+                }
+            }
+            return;
+        }
         if (NP % 2 == 0 && epi.act) {
 #pragma unroll
             for (int p = 0; p < NP; p += 2) {
@@ -1612,22 +1627,36 @@ int launch_stream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint1
 
 // nm: m-tiles of the tile space (grouped: the host's upper bound, the
 // kernel derives the actual count from the expert offsets)
-template <int BM, int WN, bool GRP>
-void launch_tiled_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
+template <int BM, int WN, bool GRP, bool EP>
+void launch_tiled_e(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
                     const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
                     const GroupArgs& ga, const Epi& epi)
 {
     const int nm = GRP ? (int)(((int64_t)ga.routed + (int64_t)ga.experts * (BM - 1)) / BM) : ceil_div(M, BM);
     const int nn = ceil_div(N, kTiledWaves * WN);
     if (pl.variant == kVariantStreamK) {
-        hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP>), dim3(pl.split), dim3(64 * kTiledWaves), 0, st, x, pw,
-                           ps, pz, y, ws, M, N, K, 0, nm, nn, 0, ga, epi);
+        hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP, EP>), dim3(pl.split), dim3(64 * kTiledWaves), 0, st, x,
+                           pw, ps, pz, y, ws, M, N, K, 0, nm, nn, 0, ga, epi);
         return;
     }
     const int nblk = nm * nn * pl.split;
     const int grid = ceil_div(nblk, 8) * 8;
-    hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP>), dim3(grid), dim3(64 * kTiledWaves), 0, st, x, pw, ps, pz,
-                       y, ws, M, N, K, pl.kgps, nm, nn, pl.split, ga, epi);
+    hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP, EP>), dim3(grid), dim3(64 * kTiledWaves), 0, st, x, pw, ps,
+                       pz, y, ws, M, N, K, pl.kgps, nm, nn, pl.split, ga, epi);
+}
+
+// A split-K launch writes raw partial sums and its reduction pass applies
+// the epilogue, so only unsplit launches need the epilogue build.
+template <int BM, int WN, bool GRP>
+void launch_tiled_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
+                    const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
+                    const GroupArgs& ga, const Epi& epi)
+{
+    const bool split = pl.variant == kVariantTiled && pl.split > 1;
+    if ((epi.bias || epi.act) && !split)
+        launch_tiled_e<BM, WN, GRP, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, ga, epi);
+    else
+        launch_tiled_e<BM, WN, GRP, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, ga, epi);
 }
 
 // Tile shapes of the grouped form.
