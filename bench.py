@@ -673,7 +673,7 @@ def main():
     evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
             for _ in points] for _ in range(psteps)]
     for s_ in range(psteps):
-        torch.cuda._sleep(5_000_000)
+        torch.cuda._sleep(40_000_000)  # ~20 ms: the host enqueues all 44 GEMMs with their events first
         step(evs[s_])
     torch.cuda.synchronize()
 

@@ -1,9 +1,12 @@
 """The five workload configurations at full size, on the launch
-configuration the benchmark times (automatic kernel choice), against the
+configurations the benchmark times (the built-in rules, and for the
+Llama-2-7B / 70B sets also the tune table bench.py loads), against the
 oracle on sampled outputs: all rows up to 64 (else 64 sampled rows) and 256
 sampled columns (the first 64, the last 64 and 128 random ones), every
 (shape, M) point.  Inputs come from workloads.py with the configurations'
 seeds and distributions."""
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -27,8 +30,23 @@ def _check_point(tag, p, x, q, z, s, M):
     assert err <= TOL, "%s M=%d: rel err %.3g" % (tag, M, err)
 
 
-@pytest.mark.parametrize("cid", [2, 3, 5])
-def test_llama_config(cid):
+TUNE_TABLE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2402_10076_amd",
+                          "tune_mi355x.txt")
+
+
+@pytest.fixture
+def bench_plans(request):
+    """The plans bench.py launches: the library's MI355X tune table for the
+    Llama-2-7B / 70B shapes (the built-in rules for everything else)."""
+    if request.param == "tuned":
+        Q.tune_table_load(TUNE_TABLE)
+    yield request.param
+    Q.tune_table_clear()
+
+
+@pytest.mark.parametrize("cid,bench_plans", [(2, "rules"), (2, "tuned"), (3, "rules"), (5, "rules"), (5, "tuned")],
+                         indirect=["bench_plans"])
+def test_llama_config(cid, bench_plans):
     cfg = W.CONFIGS[cid]
     for si, sh in enumerate(cfg.shapes):
         say("C%d %s K=%d N=%d: generating" % (cid, sh.name, sh.K, sh.N))
@@ -36,7 +54,7 @@ def test_llama_config(cid):
         q, z, s = W.draw_weights(cid, si, sh.K, sh.N)
         p = Packed(q, z, s)
         for M in sh.Ms:
-            _check_point("C%d %s" % (cid, sh.name), p, x_all[:M], q, z, s, M)
+            _check_point("C%d %s %s" % (cid, bench_plans, sh.name), p, x_all[:M], q, z, s, M)
         del p
         torch.cuda.empty_cache()
 
