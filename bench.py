@@ -186,7 +186,7 @@ def ingest_trace(trace_csv, points, dominant, out_md, command):
     s_gbs = sum(points[i]["bytes"] for i in small) / s_us / 1e3
     with open(out_md, "w") as f:
         f.write("# Kernel durations of the bench step (rocprofv3 kernel trace)\n\n")
-        f.write("Command (from the repository root on the GPU box, after `cd /tmp && export TMPDIR=/tmp`):\n\n")
+        f.write("Command (from the repository root on an MI355X, after `cd /tmp && export TMPDIR=/tmp`):\n\n")
         f.write("```\n%s\n```\n\n" % command)
         f.write("Then `python bench.py --ingest-trace <kernel_trace.csv> --trace-out <this file>` (CPU).\n\n")
         f.write("%d library dispatches = %d repetitions of the step's %d launches (eager warm-up, "
