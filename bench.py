@@ -213,6 +213,63 @@ def ingest_trace(trace_csv, points, dominant, out_md, command):
     return dom_us
 
 
+MFMA_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_F16", "SQ_BUSY_CU_CYCLES", "SQ_INSTS_LDS",
+                 "SQ_LDS_BANK_CONFLICT", "SQ_INSTS_VALU", "SQ_WAVE_CYCLES", "GRBM_GUI_ACTIVE")
+MI355X_XCDS = 8
+MI355X_SIMDS = 256 * 4
+
+
+def ingest_mfma(csv_path, points, out_md, command):
+    """Matrix-core utilisation per GEMM of the step from one rocprofv3 --pmc
+    run of MFMA_COUNTERS over this script (--steps 1 --warmup 0): busy cycles
+    of the matrix units over the GPU's active cycles times the SIMDs (the
+    profiler's MfmaUtil), the matrix operations issued against the GEMM's
+    algorithmic flops, and the LDS instruction and bank-conflict counts."""
+    import csv
+    seq = launch_sequence(points)
+    disp = {}
+    for r in csv.DictReader(open(csv_path)):
+        name = r["Kernel_Name"]
+        if "anonymous namespace)::" not in name or "at::" in name:
+            continue
+        d = disp.setdefault(int(r["Dispatch_Id"]), {"name": name})
+        d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    ids = sorted(disp)
+    names = [disp[i]["name"] for i in ids]
+    reps = whole_repetitions(names, seq)
+    if reps == 0:
+        raise SystemExit("%s: the library dispatches do not start with the step's launch sequence" % csv_path)
+    acc = [dict() for _ in points]
+    j = 0
+    for _ in range(reps):
+        for i, p in enumerate(points):
+            d = disp[ids[j]]   # the GEMM kernel itself (a split-K reduction follows it)
+            for c in MFMA_COUNTERS:
+                acc[i].setdefault(c, []).append(d.get(c, 0.0))
+            j += 2 if (p["sel"]["variant"] == 2 and p["sel"]["split_k"] > 1) else 1
+    lines = ["| cfg | shape | K | N | M | kernel | matrix busy % | matrix flops / algorithmic | LDS instr | LDS bank conflicts |",
+             "|---|---|---|---|---|---|---|---|---|---|"]
+    for i, p in enumerate(points):
+        a = {c: float(np.mean(v)) for c, v in acc[i].items()}
+        active = a["GRBM_GUI_ACTIVE"] / MI355X_XCDS
+        util = 100.0 * a["SQ_VALU_MFMA_BUSY_CYCLES"] / (active * MI355X_SIMDS) if active else 0.0
+        mflops = a["SQ_INSTS_VALU_MFMA_MOPS_F16"] * 512
+        lines.append("| C%d | %s | %d | %d | %d | %s | %.1f | %.2f | %.3g | %.3g |" % (
+            p["cid"], p["shape"], p["K"], p["N"], p["M"], p["kernel"], util, mflops / p["flops"],
+            a["SQ_INSTS_LDS"], a["SQ_LDS_BANK_CONFLICT"]))
+    with open(out_md, "w") as f:
+        f.write("# Matrix-core utilisation per GEMM of the bench step (rocprofv3 counters)\n\n")
+        f.write("Command (from the repository root on an MI355X, after `cd /tmp && export TMPDIR=/tmp`):\n\n")
+        f.write("```\n%s\n```\n\n" % command)
+        f.write("Then `python bench.py --ingest-mfma <counter_collection.csv>` (CPU). %d repetitions of the step's "
+                "launch sequence; values are means per GEMM kernel launch (the split-K reduction pass is not "
+                "included). matrix busy %% = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / %d XCDs x %d SIMDs), "
+                "the profiler's MfmaUtil; matrix flops = SQ_INSTS_VALU_MFMA_MOPS_F16 x 512 against 2MNK "
+                "(above 1 where M is padded to 16-row blocks).\n\n" % (reps, MI355X_XCDS, MI355X_SIMDS))
+        f.write("\n".join(lines) + "\n")
+    return reps
+
+
 def stored_traffic(dominant: str):
     """HBM bytes per launch from the stored counter measurement, or None when
     there is none for this kernel or the kernel source changed since."""
@@ -509,6 +566,9 @@ def main():
                     help="only measure direct-to-register vs LDS write-back of the dequantized weights")
     ap.add_argument("--ablation-only", default="", metavar="K,N,M",
                     help="with --ablation: one shape, 5 launches per mode (for counter runs)")
+    ap.add_argument("--ingest-mfma", metavar="COUNTER_CSV",
+                    help="per-GEMM matrix-core utilisation from a rocprofv3 --pmc run of MFMA_COUNTERS")
+    ap.add_argument("--mfma-out", default=os.path.join(ROOT, "profiles", "mfma_util_bench_llama2_7b_70b.md"))
     ap.add_argument("--ingest-trace", metavar="KERNEL_TRACE_CSV",
                     help="per-GEMM kernel durations from a rocprofv3 --kernel-trace run of this script")
     ap.add_argument("--trace-out", default=os.path.join(ROOT, "profiles", "bench_llama2_7b_70b_kernel_trace.md"))
@@ -533,6 +593,20 @@ def main():
             args.dominant, ingest_trace(args.ingest_trace, points, args.dominant, args.trace_out, args.trace_command)))
         return
 
+    if args.ingest_mfma:
+        import paper_2402_10076_amd as Q
+        import workloads as W
+        points = build_points([int(c) for c in args.configs.split(",") if c])
+        for p in points:
+            p["sel"] = Q.select_config(p["M"], p["N"], p["K"])
+            p["kernel"] = kernel_name(p["sel"])
+            p["flops"] = W.flops(p["M"], p["N"], p["K"])
+        cmd = ("rocprofv3 --pmc " + " ".join(MFMA_COUNTERS) + " --output-format csv -d <dir> -o m "
+               "-- python3 <repo>/bench.py --steps 1 --warmup 0 --no-cpu-baseline")
+        print("%d repetitions ingested into %s" % (ingest_mfma(args.ingest_mfma, points, args.mfma_out, cmd),
+                                                   args.mfma_out))
+        return
+
     if args.ingest_pmc:
         import paper_2402_10076_amd as Q
         points = build_points([int(c) for c in args.configs.split(",") if c])
@@ -550,8 +624,8 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py measures the single-GPU path only: this build runs on one MI355X "
-              "(--gpus 1); multi-GPU runs are not part of it.", file=sys.stderr)
+        print("bench.py measures the single-GPU path only: the library runs on one MI355X "
+              "(--gpus 1); multi-GPU runs are not implemented.", file=sys.stderr)
         sys.exit(2)
 
     import torch
