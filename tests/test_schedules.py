@@ -1,0 +1,167 @@
+"""Host-side checks of the GEMM schedules, without a GPU.
+
+* The library's own planning through the C ABI: for many shapes the
+  automatic configuration is one the explicit path accepts, and the
+  workspace the automatic path reports equals the one of that explicit
+  configuration.
+* The index arithmetic of the persistent schedules, written out the way the
+  kernels compute it: the stream-K split of tiles x k-groups, the grouped
+  form's per-expert tile table, and the balanced stream kernel's trip-aligned
+  ranges.  Each must cover every unit exactly once, give every shared tile a
+  contiguous run of contributors whose partial-slot indices agree between
+  writer and reader, and keep every access inside its buffer.  (These are the
+  checks run before each schedule first ran on a GPU.)
+"""
+import numpy as np
+import pytest
+
+import paper_2402_10076_amd as Q
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_automatic_plans_are_valid_explicit_plans(seed):
+    g = np.random.Generator(np.random.PCG64(seed))
+    for _ in range(60):
+        M = int(g.choice([1, 2, 4, 8, 9, 16, 17, 33, 64, 65, 100, 128, 200, 256, 512, 1024, 2048]))
+        N = int(g.integers(1, 512)) * 16
+        K = int(g.integers(1, 128)) * 128
+        sel = Q.select_config(M, N, K)
+        cfg = Q.make_config(**sel)
+        assert Q.workspace_bytes(M, N, K, cfg) == Q.workspace_bytes(M, N, K), (M, N, K, sel)
+        assert sel["variant"] in (Q.VARIANT_STREAM, Q.VARIANT_TILED, Q.VARIANT_STREAMK), sel
+
+
+def _owner(u, W, U):
+    """Worker owning unit u when W workers split U units as [w*U/W, (w+1)*U/W)."""
+    return ((u + 1) * W - 1) // U
+
+
+def streamk_partition(tiles, KG, G):
+    """Stream-K of the tiled kernel: G workgroups (8 <= G <= tiles*KG, a
+    multiple of 8) split tiles x KG units; returns per tile the contributor
+    list [(workgroup, slot, kb, ke)] in k order."""
+    U = tiles * KG
+    pieces = {}
+    for wid in range(G):
+        u0, u1 = wid * U // G, (wid + 1) * U // G
+        assert u1 > u0, "empty range"
+        u = u0
+        while u < u1:
+            tt, kb = divmod(u, KG)
+            ke = min(KG, kb + (u1 - u))
+            if not (kb == 0 and ke == KG):
+                slot = 2 * wid + (0 if u == u0 else 1)
+                assert slot < 2 * G
+                pieces.setdefault(tt, []).append((wid, slot, kb, ke))
+            else:
+                pieces.setdefault(tt, []).append((wid, None, 0, KG))
+            u += ke - kb
+    return pieces, U
+
+
+@pytest.mark.parametrize("tiles,KG,G", [(1, 32, 8), (3, 7, 16), (40, 64, 256), (256, 224, 256), (320, 64, 256),
+                                         (17, 9, 152), (5, 200, 1000)])
+def test_streamk_contributors_and_slots(tiles, KG, G):
+    G = min(G, tiles * KG) // 8 * 8
+    pieces, U = streamk_partition(tiles, KG, G)
+    assert sorted(pieces) == list(range(tiles))
+    for t, ps in pieces.items():
+        # the k-ranges of a tile's pieces tile [0, KG) in contributor order
+        assert [p[2] for p in ps][0] == 0 and ps[-1][3] == KG
+        assert all(a[3] == b[2] for a, b in zip(ps, ps[1:]))
+        if len(ps) == 1:
+            continue
+        tb = t * KG
+        w0, w1 = _owner(tb, G, U), _owner(tb + KG - 1, G, U)
+        assert [p[0] for p in ps] == list(range(w0, w1 + 1)), "contributors are consecutive"
+        for wid, slot, _, _ in ps:
+            # the reader's rule for a contributor's slot
+            assert slot == 2 * wid + (0 if wid * U // G >= tb else 1)
+
+
+def grouped_tiles(offsets, R, BM, nn):
+    """The grouped kernel's tile table (clamped offsets, per-expert m-tile
+    counts, prefix sums) and its tile -> (expert, m0, mend, n-tile) map."""
+    E = len(offsets) - 1
+    lo, hi, cum = [], [], [0]
+    for e in range(E):
+        a = min(max(offsets[e], 0), R)
+        b = min(max(offsets[e + 1], a), R)
+        lo.append(a), hi.append(b), cum.append(cum[-1] + (b - a + BM - 1) // BM)
+
+    def tile(t):
+        a, b = 0, E
+        while b - a > 1:
+            mid = (a + b) // 2
+            if cum[mid] * nn <= t:
+                a = mid
+            else:
+                b = mid
+        e = a
+        local = t - cum[e] * nn
+        te = cum[e + 1] - cum[e]
+        nt = local // te
+        m0 = lo[e] + (local - nt * te) * BM
+        return e, m0, hi[e], nt
+    return cum[E], tile
+
+
+@pytest.mark.parametrize("counts,BM", [([130, 149, 111, 127, 132, 133, 122, 120], 128), ([0, 0, 5, 0], 16),
+                                        ([37, 0, 129, 1, 66], 64), ([1], 32), ([3] * 300, 16)])
+def test_grouped_tile_table_covers_every_row_once(counts, BM):
+    offsets = np.concatenate([[0], np.cumsum(counts)]).tolist()
+    R = offsets[-1]
+    nn = 3
+    n_mt, tile = grouped_tiles(offsets, R, BM, nn)
+    assert n_mt <= (R + len(counts) * (BM - 1)) // BM, "host upper bound of m-tiles"
+    seen = np.zeros((R, nn), np.int64)
+    for t in range(n_mt * nn):
+        e, m0, mend, nt = tile(t)
+        assert offsets[e] <= m0 < mend <= offsets[e + 1] and nt < nn
+        seen[m0:min(m0 + BM, mend), nt] += 1
+    assert np.all(seen == 1)
+
+
+def test_grouped_tile_table_clamps_malformed_offsets():
+    """Decreasing or out-of-range offsets stay inside [0, R)."""
+    R, BM, nn = 50, 16, 2
+    for offsets in ([0, 70, 20, 50], [-5, 10, 10, 99], [0, 50, 40, 30]):
+        n_mt, tile = grouped_tiles(offsets, R, BM, nn)
+        for t in range(n_mt * nn):
+            e, m0, mend, nt = tile(t)
+            assert 0 <= m0 < mend <= R
+
+
+def bstream_ranges(U, D, W):
+    UD = U // D
+    W = min(W, UD)
+    return W, [(w * UD // W * D, (w + 1) * UD // W * D) for w in range(W)]
+
+
+@pytest.mark.parametrize("NT,KG,G", [(3, 16, 1), (17, 32, 1), (5, 48, 3), (3584, 64, 256), (512, 224, 256),
+                                      (640, 64, 512), (2, 16, 64)])
+def test_bstream_ranges_pieces_and_slots(NT, KG, G):
+    D = 16
+    U = NT * KG
+    W, ranges = bstream_ranges(U, D, G * 8)
+    UD = U // D
+    covered = np.zeros(U, np.int64)
+    slots = {}
+    for gw, (u0, u1) in enumerate(ranges):
+        assert u1 > u0 and u0 % D == 0 and u1 % D == 0
+        covered[u0:u1] += 1
+        nt, pstart = u0 // KG, u0
+        for u in range(u0, u1):
+            if u % KG == KG - 1 or u == u1 - 1:
+                if not (pstart == nt * KG and u == nt * KG + KG - 1):
+                    slots[(nt, gw)] = 2 * gw + (0 if pstart == u0 else 1)
+                pstart = u + 1
+                if u % KG == KG - 1:
+                    nt += 1
+    assert np.all(covered == 1)
+    for (t, gw), slot in slots.items():
+        tb = t * KG
+        w0 = ((tb // D + 1) * W - 1) // UD
+        w1 = (((tb + KG - 1) // D + 1) * W - 1) // UD
+        assert w0 <= gw <= w1 < W
+        assert slot == 2 * gw + (0 if (gw * UD // W) * D >= tb else 1)
