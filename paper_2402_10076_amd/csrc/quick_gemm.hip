@@ -482,13 +482,16 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 //
 // Weights: one 16-byte load per lane and n-tile per k-group into a ring of
 // NST register slots.  k-group k+NST-1 (activations and weights) is requested
-// while k-group k is computed; the end-of-k-group wait only drains the loads
+// while k-group k is computed; the wait of k-group k only drains the loads
 // of k-group k+1 (vector-memory counters retire in issue order), so NST-2
 // k-groups stay in flight across the barrier.
 //
 // Inside a k-group: 4 steps of 32 channels, software-pipelined -- while the
 // matrix instructions of step j run, the activation fragments of step j+1
-// are read from LDS and the weights of step j+1 are dequantized.
+// are read from LDS and the weights of step j+1 are dequantized.  The
+// pipeline runs on across k-groups: the wait and the workgroup barrier of
+// k-group k come before its last step, whose matrix instructions then cover
+// the fragment reads and dequant of k-group k+1's first step.
 //
 // Tiles are numbered M-fastest and assigned so that consecutive numbers run
 // on the same XCD (workgroup ids go to the 8 XCDs round-robin): M-tiles that
@@ -726,12 +729,18 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     auto wb_at = [&](int p, int j) -> uint8_t* {
         return lds_wb + ((size_t)(wave * NP * 16 + p * 16 + c) * WB_RS + 32 * j + 8 * g) * 2;
     };
-    auto kgroup = [&](int st) __attribute__((always_inline)) {
-        Deq d[NP];
+
+    // Fragments carried from one k-group to the next: the barrier of a
+    // k-group sits before its last k-step, and that step's matrix
+    // instructions cover the LDS fragment reads and the dequant of the next
+    // k-group's first step, so no k-group starts with the matrix units
+    // waiting on LDS latency behind a barrier.
+    h8_t fa[2][NP];    // weights (A operand), double-buffered over k-steps
+    h8_t fb[2][MTT];   // activations (B operand)
+    Deq dcur[NP];      // dequant constants of the current k-group
+    auto make_d = [&](int st, Deq (&d)[NP]) __attribute__((always_inline)) {
 #pragma unroll
         for (int p = 0; p < NP; ++p) d[p] = make_deq(sr[st][p], (zr[st][p] >> (4 * (c & 7))) & 15u);
-        h8_t a[2][NP];
-        h8_t b[2][MTT];
         if constexpr (WB != 0) {
             // the conventional order: dequantize the whole k-group of weights
             // into the LDS tile first (same-wave LDS operations stay ordered)
@@ -741,34 +750,60 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
                 for (int j = 0; j < 4; ++j)
                     *reinterpret_cast<h8_t*>(wb_at(p, j)) = dequant8(wr[st][p][j], d[p]);
         }
-        auto afrag = [&](int p, int j) -> h8_t {
-            if constexpr (WB != 0) return *reinterpret_cast<const h8_t*>(wb_at(p, j));
-            else return dequant8(wr[st][p][j], d[p]);
-        };
+    };
+    auto afrag = [&](int st, int p, int j, const Deq (&d)[NP]) -> h8_t {
+        if constexpr (WB != 0) return *reinterpret_cast<const h8_t*>(wb_at(p, j));
+        else return dequant8(wr[st][p][j], d[p]);
+    };
+    auto load_step0 = [&](int st) __attribute__((always_inline)) {
+        make_d(st, dcur);
 #pragma unroll
-        for (int p = 0; p < NP; ++p) a[0][p] = afrag(p, 0);
+        for (int p = 0; p < NP; ++p) fa[0][p] = afrag(st, p, 0, dcur);
 #pragma unroll
-        for (int mt = 0; mt < MTT; ++mt) b[0][mt] = bfrag(st, mt, 0);
+        for (int mt = 0; mt < MTT; ++mt) fb[0][mt] = bfrag(st, mt, 0);
+    };
+    // One k-group on stage / ring slot st, its step-0 fragments already in
+    // fa[0], fb[0].  At its barrier at most `wgroups` k-groups of this wave's
+    // loads stay in flight; `next`: a k-group follows in slot st+1.
+    auto kgroup = [&](int st, int wgroups, bool next) __attribute__((always_inline)) {
+        const int sn = (st + 1) % NST;
+        Deq dn[NP];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int cu = j & 1, nx = cu ^ 1;
+            if (j == 3 && next) make_d(sn, dn);
 #pragma unroll
             for (int mt = 0; mt < MTT; ++mt) {
 #pragma unroll
-                for (int p = 0; p < NP; ++p) acc[p][mt] = mfma16(a[cu][p], b[cu][mt], acc[p][mt]);
-                if (j < 3) b[nx][mt] = bfrag(st, mt, j + 1);
+                for (int p = 0; p < NP; ++p) acc[p][mt] = mfma16(fa[cu][p], fb[cu][mt], acc[p][mt]);
+                if (j < 3) fb[nx][mt] = bfrag(st, mt, j + 1);
+                else if (next) fb[nx][mt] = bfrag(sn, mt, 0);
             }
             if (j < 3) {
 #pragma unroll
-                for (int p = 0; p < NP; ++p) a[nx][p] = afrag(p, j + 1);
-                constexpr int VPER = (13 * NP + MTT - 1) / MTT;  // dequant VALU ops per block
+                for (int p = 0; p < NP; ++p) fa[nx][p] = afrag(st, p, j + 1, dcur);
+            } else if (next) {
 #pragma unroll
-                for (int mt = 0; mt < MTT; ++mt) {
-                    __builtin_amdgcn_sched_group_barrier(0x008, NP, 0);   // matrix
-                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // LDS read
-                    __builtin_amdgcn_sched_group_barrier(0x002, VPER, 0); // VALU
-                }
+                for (int p = 0; p < NP; ++p) fa[nx][p] = afrag(sn, p, 0, dn);
             }
+            constexpr int VPER = (13 * NP + MTT - 1) / MTT;  // dequant VALU ops per block
+#pragma unroll
+            for (int mt = 0; mt < MTT; ++mt) {
+                __builtin_amdgcn_sched_group_barrier(0x008, NP, 0);   // matrix
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);    // LDS read
+                __builtin_amdgcn_sched_group_barrier(0x002, VPER, 0); // VALU
+            }
+            if (j == 2) {
+                // k-group st+1 has landed for every wave, and no wave reads
+                // stage st-1 any more (its last reads came before this point)
+                wait_groups(wgroups);
+                barrier();
+                sched_fence();
+            }
+        }
+        if (next) {
+#pragma unroll
+            for (int p = 0; p < NP; ++p) dcur[p] = dn[p];
         }
     };
 
@@ -784,18 +819,18 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
             if (kb + i < ke) fetch(i, kb + i);
         wait_groups(min(NST - 2, ke - kb - 1));
         barrier();
+        sched_fence();
+        load_step0(0);
 
         // steady state: straight-line body (unconditional requests) so the
-        // compiler's own wait analysis keeps the requested k-groups in flight
+        // compiler's own wait analysis keeps the requested k-groups in flight;
+        // k-group kg+i+NST-1 goes into the slot k-group kg+i-1 left
         int kg = kb;
         for (; kg + 2 * NST - 1 <= ke; kg += NST) {
 #pragma unroll
             for (int i = 0; i < NST; ++i) {
                 fetch((i + NST - 1) % NST, kg + i + NST - 1);
-                kgroup(i);
-                // k-group kg+i+1 must have landed; later ones stay in flight
-                wait_groups(NST - 2);
-                barrier();
+                kgroup(i, NST - 2, true);
             }
         }
         // tail
@@ -805,9 +840,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
                 const int k = kg + i;
                 if (k < ke) {
                     if (k + NST - 1 < ke) fetch((i + NST - 1) % NST, k + NST - 1);
-                    kgroup(i);
-                    wait_groups(min(NST - 2, ke - k - 2));
-                    barrier();
+                    kgroup(i, min(NST - 2, ke - k - 2), k + 1 < ke);
                 }
             }
         }
