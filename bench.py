@@ -89,6 +89,18 @@ def read_counter_csv(path: str, counter: str):
     return rows
 
 
+def dominant_kernel(points_json: str, default: str) -> str:
+    """The kernel with the most per-GEMM event time in a bench run's
+    --points-out file (how the bench itself picks its dominant kernel);
+    `default` when there is no such file."""
+    if not points_json or not os.path.exists(points_json):
+        return default
+    tot = {}
+    for p in json.load(open(points_json)):
+        tot[p["kernel"]] = tot.get(p["kernel"], 0.0) + p["ms"]
+    return max(tot, key=tot.get)
+
+
 def whole_repetitions(names, seq):
     """How many times the launch sequence `seq` repeats at the start of the
     dispatched kernel `names`."""
@@ -551,7 +563,9 @@ def main():
     ap.add_argument("--ingest-pmc", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "CAL_FETCH_CSV", "CAL_WRITE_CSV"),
                     help="turn rocprofv3 FETCH_SIZE / WRITE_SIZE runs of one step (--steps 1 --warmup 0) and "
                          "of --copy-calibration into the stored HBM traffic of the dominant kernel")
-    ap.add_argument("--dominant", default="tiled_kernel<128,32>+streamK(G=256)", help="kernel name for --ingest-pmc/--ingest-trace")
+    ap.add_argument("--dominant", default="",
+                    help="kernel name for --ingest-pmc/--ingest-trace (default: the dominant kernel of the "
+                         "--points-out file of the profiled bench run)")
     ap.add_argument("--compare-fp16", action="store_true",
                     help="only compare the W4A16 GEMM with an fp16 GEMM through torch (hipBLASLt) on the "
                          "8192x8192 Llama-2-70B o_proj shape over M (context, not the metric)")
@@ -580,6 +594,8 @@ def main():
         import paper_2402_10076_amd as Q
         Q.tune_table_load(args.tune_table)
 
+    if args.ingest_trace or args.ingest_pmc:
+        args.dominant = args.dominant or dominant_kernel(args.points_out, "tiled_kernel<128,32>")
     if args.ingest_trace:
         import paper_2402_10076_amd as Q
         import workloads as W
