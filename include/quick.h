@@ -168,7 +168,10 @@ int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config_t* cfg);
  * table, keyed by (M, N, K).  From then on quick_w4a16_gemm, and the
  * automatic choice of quick_w4a16_gemm_ex / quick_workspace_bytes /
  * quick_select_config, use the recorded configuration for that shape on
- * every device.  Blocking: synchronizes `stream`; takes a few milliseconds
+ * every device.  The timings repeat launches on the caller's buffers, so
+ * a shape whose weights fit in the Infinity Cache (256 MB) is timed with its
+ * weights cache-resident rather than streaming from HBM.
+ * Blocking: synchronizes `stream`; takes a few milliseconds
  * to a few hundred for large shapes; may grow the internal workspace, so
  * not for use under graph capture.  `best` (may be NULL) receives the
  * configuration recorded.  M == 0 records nothing.
