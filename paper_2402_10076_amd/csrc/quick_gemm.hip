@@ -210,6 +210,27 @@ __device__ __forceinline__ void dma16(rsrc_t r, void* dst, uint32_t voff, uint32
 }
 // Wait until every outstanding memory operation of this wave has completed.
 __device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0); }
+// Wait until at most V vector-memory loads of this wave are outstanding
+// (V clamped to the 6-bit counter; gfx9 encoding: vmcnt in bits 3:0 and
+// 15:14, expcnt and lgkmcnt left at their maxima).
+template <int V>
+__device__ __forceinline__ void wait_vm()
+{
+    constexpr int v = V < 63 ? V : 63;
+    __builtin_amdgcn_s_waitcnt(0x0F70 | (v & 15) | ((v >> 4) << 14));
+}
+// f(std::integral_constant<int, n>{}) for a wave-uniform 0 <= n <= N: code
+// specialised on a count known only at run time.
+template <int N, class F>
+__device__ __forceinline__ void with_count(int n, F&& f)
+{
+    if constexpr (N == 0) {
+        f(std::integral_constant<int, 0>{});
+    } else {
+        if (n >= N) f(std::integral_constant<int, N>{});
+        else with_count<N - 1>(n, f);
+    }
+}
 // Workgroup execution barrier without memory-fence semantics.  Used where
 // explicit counter waits already order the memory traffic: every LDS-DMA a
 // wave issued for the next stage has completed (its vmcnt wait) and every LDS
@@ -377,37 +398,65 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         }
     };
 
+    if (XL && nk <= D) {
+        // The whole k-range fits the ring: one pass, specialised on the unit
+        // count so that every load is unconditional.  The compiler's wait
+        // before each unit then covers only that unit's loads, and units are
+        // multiplied as they land instead of after the last one.
+        with_count<D>(nk, [&](auto nkc) {
+            constexpr int NKC = decltype(nkc)::value;
 #pragma unroll
-    for (int i = 0; i < D; ++i)
-        if (kb + i < ke) load_w(ring[i], kb + i);
-    if constexpr (XL) wait_all();  // the slice has landed (weights too, once)
-    if (kb < ke) load_x(xf[0], kb);
+            for (int i = 0; i < NKC; ++i) {
+                load_w(ring[i], kb + i);
+                sched_fence();  // issue stage by stage, so each unit's loads land together
+            }
+            if constexpr (NKC > 0) {
+                // the slice copy was issued before these 3 * NPW * NKC loads
+                wait_vm<3 * NPW * NKC>();
+                load_x(xf[0], kb);
+#pragma unroll
+                for (int i = 0; i < NKC; ++i) {
+                    if (i + 1 < NKC) load_x(xf[(i + 1) & 1], kb + i + 1);
+                    compute(ring[i], xf[i & 1]);
+                    // no work of a later unit moves up here, where it would
+                    // wait for that unit's loads
+                    sched_fence();
+                }
+            }
+        });
+    } else {
+#pragma unroll
+        for (int i = 0; i < D; ++i)
+            if (kb + i < ke) load_w(ring[i], kb + i);
+        if constexpr (XL) wait_all();  // the slice has landed (weights too, once)
+        if (kb < ke) load_x(xf[0], kb);
 
-    // steady state: straight-line body with unconditional requests, so the
-    // compiler's wait analysis keeps D-1 stages in flight instead of
-    // draining the ring at every trip
-    int kg = kb;
-    for (; kg + 2 * D <= ke; kg += D) {
+        // steady state: straight-line body with unconditional requests, so
+        // the compiler's wait analysis keeps D-1 stages in flight instead of
+        // draining the ring at every trip
+        int kg = kb;
+        for (; kg + 2 * D <= ke; kg += D) {
 #pragma unroll
-        for (int i = 0; i < D; ++i) {
-            load_x(xf[(i + 1) & 1], kg + i + 1);
-            compute(ring[i], xf[i & 1]);
-            load_w(ring[i], kg + i + D);
-            // keep each refill where it is: the scheduler would otherwise
-            // sink all of them to the end of the trip and issue them in one
-            // burst that the next trip then waits for
-            sched_fence();
-        }
-    }
-    // tail
-    for (; kg < ke; kg += D) {
-#pragma unroll
-        for (int i = 0; i < D; ++i) {
-            const int k = kg + i;
-            if (k < ke) {
-                if (k + 1 < ke) load_x(xf[(i + 1) & 1], k + 1);
+            for (int i = 0; i < D; ++i) {
+                load_x(xf[(i + 1) & 1], kg + i + 1);
                 compute(ring[i], xf[i & 1]);
-                if (k + D < ke) load_w(ring[i], k + D);
+                load_w(ring[i], kg + i + D);
+                // keep each refill where it is: the scheduler would otherwise
+                // sink all of them to the end of the trip and issue them in
+                // one burst that the next trip then waits for
+                sched_fence();
+            }
+        }
+        // tail
+        for (; kg < ke; kg += D) {
+#pragma unroll
+            for (int i = 0; i < D; ++i) {
+                const int k = kg + i;
+                if (k < ke) {
+                    if (k + 1 < ke) load_x(xf[(i + 1) & 1], k + 1);
+                    compute(ring[i], xf[i & 1]);
+                    if (k + D < ke) load_w(ring[i], k + D);
+                }
             }
         }
     }
