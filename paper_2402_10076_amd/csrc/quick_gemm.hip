@@ -289,6 +289,7 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
               uint16_t* __restrict__ y, int M, int N, int K, Epi epi)
 {
     static_assert(D % 2 == 0, "ring depth must be even (activation double buffer parity)");
+    static_assert(!XL || 3 * NPW * D <= 63, "the slice-copy waits count the ring's loads within the 6-bit vmcnt");
     extern __shared__ __attribute__((aligned(16))) uint8_t xlds[];
     const int KG = K >> 7;
     const int NT = N >> 4;
@@ -425,27 +426,42 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
             }
         });
     } else {
-#pragma unroll
-        for (int i = 0; i < D; ++i)
-            if (kb + i < ke) load_w(ring[i], kb + i);
-        if constexpr (XL) wait_all();  // the slice has landed (weights too, once)
-        if (kb < ke) load_x(xf[0], kb);
-
-        // steady state: straight-line body with unconditional requests, so
-        // the compiler's wait analysis keeps D-1 stages in flight instead of
-        // draining the ring at every trip
-        int kg = kb;
-        for (; kg + 2 * D <= ke; kg += D) {
+        // one trip of the ring: unit k0 + i is multiplied while unit
+        // k0 + i + D is requested
+        auto trip = [&](int k0) {
 #pragma unroll
             for (int i = 0; i < D; ++i) {
-                load_x(xf[(i + 1) & 1], kg + i + 1);
+                load_x(xf[(i + 1) & 1], k0 + i + 1);
                 compute(ring[i], xf[i & 1]);
-                load_w(ring[i], kg + i + D);
+                load_w(ring[i], k0 + i + D);
                 // keep each refill where it is: the scheduler would otherwise
                 // sink all of them to the end of the trip and issue them in
                 // one burst that the next trip then waits for
                 sched_fence();
             }
+        };
+        int kg = kb;
+        if (nk >= 2 * D) {
+            // At least one full trip.  Unconditional requests, the first
+            // activation fragments ahead of the weights, and the first trip
+            // peeled: the loop is then entered in the state it loops back in
+            // (D stages in flight), and the compiler's wait analysis keeps
+            // D-1 stages in flight from the first unit on.
+            if constexpr (!XL) load_x(xf[0], kb);
+#pragma unroll
+            for (int i = 0; i < D; ++i) load_w(ring[i], kb + i);
+            if constexpr (XL) {
+                wait_vm<3 * NPW * D>();  // the slice copy, issued before these loads, has landed
+                load_x(xf[0], kb);
+            }
+            trip(kg);
+            for (kg += D; kg + 2 * D <= ke; kg += D) trip(kg);
+        } else {
+#pragma unroll
+            for (int i = 0; i < D; ++i)
+                if (kb + i < ke) load_w(ring[i], kb + i);
+            if constexpr (XL) wait_all();  // the slice has landed (weights too, once)
+            if (kb < ke) load_x(xf[0], kb);
         }
         // tail
         for (; kg < ke; kg += D) {
