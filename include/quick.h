@@ -163,17 +163,19 @@ int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config_t* cfg);
 /* Times every supported kernel configuration for this shape on the caller's
  * buffers (same arguments and contract as quick_w4a16_gemm; y is
  * overwritten, the last write coming from the best configuration) with HIP
- * events on `stream` (per configuration the fastest of three timings of five
- * launches), and records the fastest in the process-wide tune
+ * events on `stream` (per configuration the fastest of three timings of
+ * max(5, copies) launches), and records the fastest in the process-wide tune
  * table, keyed by (M, N, K).  From then on quick_w4a16_gemm, and the
  * automatic choice of quick_w4a16_gemm_ex / quick_workspace_bytes /
  * quick_select_config, use the recorded configuration for that shape on
- * every device.  The timings repeat launches on the caller's buffers, so
- * a shape whose weights fit in the Infinity Cache (256 MB) is timed with its
- * weights cache-resident rather than streaming from HBM.
- * Blocking: synchronizes `stream`; takes a few milliseconds
- * to a few hundred for large shapes; may grow the internal workspace, so
- * not for use under graph capture.  `best` (may be NULL) receives the
+ * every device.  The timed launches rotate through temporary device copies
+ * of packed, scales and zeros spanning at least 512 MB (twice the 256 MB
+ * Infinity Cache, at most 64 copies), so that each launch streams its
+ * weights from HBM as in a forward pass; when that memory cannot be
+ * allocated, they repeat the caller's buffers.
+ * Blocking: synchronizes `stream`; takes tens of milliseconds to a few
+ * hundred; allocates and frees the copies and may grow the internal
+ * workspace, so not for use under graph capture.  `best` (may be NULL) receives the
  * configuration recorded.  M == 0 records nothing.
  * Errors: as quick_w4a16_gemm. */
 int quick_tune(const void* x, const void* packed, const void* scales, const void* zeros, void* y,

@@ -1980,6 +1980,12 @@ std::vector<quick_config_t> tune_candidates(int64_t M, int64_t K)
 
 }  // namespace
 
+// Timed launches of quick_tune rotate through device copies of the weights
+// spanning at least this many bytes (twice the 256 MB Infinity Cache), so
+// that each launch streams its weights from HBM as in a forward pass.
+constexpr size_t kTuneSpan = (size_t)512 << 20;
+constexpr int kTuneMaxCopies = 64;
+
 extern "C" int quick_tune(const void* x, const void* packed, const void* scales, const void* zeros, void* y,
                           int64_t M, int64_t N, int64_t K, int64_t group, void* stream, quick_config_t* best)
 {
@@ -1992,23 +1998,53 @@ extern "C" int quick_tune(const void* x, const void* packed, const void* scales,
         if (e0) (void)hipEventDestroy(e0);
         return QUICK_ERR_HIP;
     }
-    constexpr int kReps = 5;
+    // weight copies: copy 0 is the caller's; the others live in one
+    // temporary allocation (none when it cannot be had: then the timings
+    // repeat the caller's buffers)
+    const size_t wb = (size_t)K * N / 2, sb = wb / 32, zb = wb / 128;
+    auto al = [](size_t b) { return (b + 255) / 256 * 256; };
+    const size_t per = al(wb) + al(sb) + al(zb);
+    int ncopy = (int)std::min<size_t>(kTuneMaxCopies, std::max<size_t>(1, (kTuneSpan + per - 1) / per));
+    uint8_t* extra = nullptr;
+    if (ncopy > 1 && hipMalloc(&extra, (size_t)(ncopy - 1) * per) != hipSuccess) {
+        (void)hipGetLastError();
+        extra = nullptr;
+        ncopy = 1;
+    }
+    std::vector<const void*> cw(ncopy, packed), cs(ncopy, scales), cz(ncopy, zeros);
+    for (int i = 1; i < ncopy && !st; ++i) {
+        uint8_t* b = extra + (size_t)(i - 1) * per;
+        cw[i] = b;
+        cs[i] = b + al(wb);
+        cz[i] = b + al(wb) + al(sb);
+        if (hipMemcpyAsync((void*)cw[i], packed, wb, hipMemcpyDeviceToDevice, hs) != hipSuccess ||
+            hipMemcpyAsync((void*)cs[i], scales, sb, hipMemcpyDeviceToDevice, hs) != hipSuccess ||
+            hipMemcpyAsync((void*)cz[i], zeros, zb, hipMemcpyDeviceToDevice, hs) != hipSuccess)
+            st = QUICK_ERR_HIP;
+    }
+    const int reps = std::max(5, ncopy);
     constexpr int kTrials = 3;
     float best_ms = 0.f;
     quick_config_t bestc{};
     bool found = false;
     for (const quick_config_t& c : tune_candidates(M, K)) {
-        st = gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, &c, nullptr, 0);  // warm-up
-        if (st == QUICK_ERR_INVALID_ARG) continue;  // not supported for this shape
         if (st) break;
-        // the fastest of kTrials timings of kReps launches: a single timing
+        st = gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, &c, nullptr, 0);  // warm-up
+        if (st == QUICK_ERR_INVALID_ARG) {  // not supported for this shape
+            st = QUICK_OK;
+            continue;
+        }
+        if (st) break;
+        // the fastest of kTrials timings of `reps` launches: a single timing
         // can catch a clock or memory hiccup and record a slow configuration
         float ms = 0.f;
         for (int t = 0; t < kTrials && !st; ++t) {
             float tm = 0.f;
             if (hipEventRecord(e0, hs) != hipSuccess) { st = QUICK_ERR_HIP; break; }
-            for (int r = 0; r < kReps && !st; ++r)
-                st = gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, &c, nullptr, 0);
+            for (int r = 0; r < reps && !st; ++r) {
+                const int i = r % ncopy;
+                st = gemm_impl(x, cw[i], cs[i], cz[i], y, M, N, K, group, stream, &c, nullptr, 0);
+            }
             if (st) break;
             if (hipEventRecord(e1, hs) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
                 hipEventElapsedTime(&tm, e0, e1) != hipSuccess) {
@@ -2026,6 +2062,11 @@ extern "C" int quick_tune(const void* x, const void* packed, const void* scales,
     }
     (void)hipEventDestroy(e0);
     (void)hipEventDestroy(e1);
+    if (extra) {
+        // the copies may still be read by launches in flight
+        if (hipStreamSynchronize(hs) != hipSuccess && !st) st = QUICK_ERR_HIP;
+        (void)hipFree(extra);
+    }
     if (st) return st;
     if (!found) return QUICK_ERR_INVALID_ARG;
     {

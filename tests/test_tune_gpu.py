@@ -1,5 +1,5 @@
-"""quick_tune: times the configurations of a shape on the caller's buffers,
-records the fastest, and the automatic path then uses it."""
+"""quick_tune: times the configurations of a shape (rotating through copies of
+the caller's weights), records the fastest, and the automatic path then uses it."""
 import numpy as np
 import pytest
 import torch
