@@ -44,6 +44,19 @@ def test_stream_variants(M, cfg):
         _check(M, K, N, cfg, seed=M * 1000 + K + N)
 
 
+@pytest.mark.parametrize("waves,npw", [(1, 1), (1, 2), (4, 1), (4, 2)])
+@pytest.mark.parametrize("M", [1, 3, 16])
+def test_stream_ring_regimes(M, waves, npw):
+    """Per-wave k-ranges on both sides of every register-ring depth the stream
+    kernel uses (D = 4, 8, 16): a single pass (up to D units), one partial
+    trip (D+1 .. 2D-1), and the peeled first trip plus the steady loop and a
+    ragged tail (2D and more); activations staged in LDS (small M*K) or
+    loaded from L2."""
+    cfg = dict(variant=1, split_k=waves, tile_n=npw)
+    for units in (3, 4, 5, 7, 8, 9, 15, 16, 17, 31, 32, 35, 69):
+        _check(M, 128 * units * waves, 48, cfg, seed=units * 10 + M)
+
+
 @pytest.mark.parametrize("cfg", TILED_CFGS, ids=lambda c: "bm%d_wn%d_s%d" % (c["tile_m"], c["tile_n"], c["split_k"]))
 @pytest.mark.parametrize("M", [1, 65, 129, 300])
 def test_tiled_variants(M, cfg):
