@@ -164,7 +164,7 @@ int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config_t* cfg);
  * buffers (same arguments and contract as quick_w4a16_gemm; y is
  * overwritten, the last write coming from the best configuration) with HIP
  * events on `stream` (per configuration the fastest of three timings of
- * max(5, copies) launches), and records the fastest in the process-wide tune
+ * max(10, copies) launches), and records the fastest in the process-wide tune
  * table, keyed by (M, N, K).  From then on quick_w4a16_gemm, and the
  * automatic choice of quick_w4a16_gemm_ex / quick_workspace_bytes /
  * quick_select_config, use the recorded configuration for that shape on

@@ -282,6 +282,10 @@ struct WStage {
     uint32_t z[NPW];
 };
 
+// Units the stream kernel's single pass keeps requested ahead of the one it
+// multiplies.
+constexpr int kStreamLookahead = 4;
+
 template <int MT, int NPW, int WAVES, int D, bool XL>
 __global__ void __launch_bounds__(64 * WAVES)
 stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
@@ -406,19 +410,24 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         // multiplied as they land instead of after the last one.
         with_count<D>(nk, [&](auto nkc) {
             constexpr int NKC = decltype(nkc)::value;
+            // LA units ahead: requests beyond that would only queue behind
+            // the bandwidth-bound ones already in flight while holding back
+            // the first multiplications (in-order issue)
+            constexpr int LA = NKC < kStreamLookahead ? NKC : kStreamLookahead;
 #pragma unroll
-            for (int i = 0; i < NKC; ++i) {
+            for (int i = 0; i < LA; ++i) {
                 load_w(ring[i], kb + i);
                 sched_fence();  // issue stage by stage, so each unit's loads land together
             }
             if constexpr (NKC > 0) {
-                // the slice copy was issued before these 3 * NPW * NKC loads
-                wait_vm<3 * NPW * NKC>();
+                // the slice copy was issued before these 3 * NPW * LA loads
+                wait_vm<3 * NPW * LA>();
                 load_x(xf[0], kb);
 #pragma unroll
                 for (int i = 0; i < NKC; ++i) {
                     if (i + 1 < NKC) load_x(xf[(i + 1) & 1], kb + i + 1);
                     compute(ring[i], xf[i & 1]);
+                    if (i + LA < NKC) load_w(ring[i + LA], kb + i + LA);
                     // no work of a later unit moves up here, where it would
                     // wait for that unit's loads
                     sched_fence();
@@ -2002,7 +2011,9 @@ extern "C" int quick_tune(const void* x, const void* packed, const void* scales,
     // temporary allocation (none when it cannot be had: then the timings
     // repeat the caller's buffers)
     const size_t wb = (size_t)K * N / 2, sb = wb / 32, zb = wb / 128;
-    auto al = [](size_t b) { return (b + 255) / 256 * 256; };
+    // 2 MiB-aligned like the caller's allocations, so that every copy maps
+    // onto the memory channels as the original does
+    auto al = [](size_t b) { return (b + ((size_t)2 << 20) - 1) / ((size_t)2 << 20) * ((size_t)2 << 20); };
     const size_t per = al(wb) + al(sb) + al(zb);
     int ncopy = (int)std::min<size_t>(kTuneMaxCopies, std::max<size_t>(1, (kTuneSpan + per - 1) / per));
     uint8_t* extra = nullptr;
@@ -2022,7 +2033,7 @@ extern "C" int quick_tune(const void* x, const void* packed, const void* scales,
             hipMemcpyAsync((void*)cz[i], zeros, zb, hipMemcpyDeviceToDevice, hs) != hipSuccess)
             st = QUICK_ERR_HIP;
     }
-    const int reps = std::max(5, ncopy);
+    const int reps = std::max(10, ncopy);
     constexpr int kTrials = 3;
     float best_ms = 0.f;
     quick_config_t bestc{};
