@@ -282,8 +282,10 @@ struct WStage {
     uint32_t z[NPW];
 };
 
-// Units the stream kernel's single pass keeps requested ahead of the one it
+// Longest per-wave k-range (units) the stream kernel runs as one specialised
+// pass, and the units that pass keeps requested ahead of the one it
 // multiplies.
+constexpr int kStreamSinglePass = 16;
 constexpr int kStreamLookahead = 4;
 
 template <int MT, int NPW, int WAVES, int D, bool XL>
@@ -403,20 +405,22 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         }
     };
 
-    if (XL && nk <= D) {
-        // The whole k-range fits the ring: one pass, specialised on the unit
-        // count so that every load is unconditional.  The compiler's wait
-        // before each unit then covers only that unit's loads, and units are
-        // multiplied as they land instead of after the last one.
-        with_count<D>(nk, [&](auto nkc) {
+    if (XL && nk <= kStreamSinglePass) {
+        // A short k-range: one pass, specialised on the unit count so that
+        // every load is unconditional.  The compiler's wait before each unit
+        // then covers only that unit's loads, and units are multiplied as
+        // they land instead of after the last one.
+        with_count<kStreamSinglePass>(nk, [&](auto nkc) {
             constexpr int NKC = decltype(nkc)::value;
             // LA units ahead: requests beyond that would only queue behind
             // the bandwidth-bound ones already in flight while holding back
             // the first multiplications (in-order issue)
             constexpr int LA = NKC < kStreamLookahead ? NKC : kStreamLookahead;
+            constexpr int R = LA + 1;  // stages live at once
+            WStage<NPW> sring[R];
 #pragma unroll
             for (int i = 0; i < LA; ++i) {
-                load_w(ring[i], kb + i);
+                load_w(sring[i], kb + i);
                 sched_fence();  // issue stage by stage, so each unit's loads land together
             }
             if constexpr (NKC > 0) {
@@ -426,8 +430,8 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 #pragma unroll
                 for (int i = 0; i < NKC; ++i) {
                     if (i + 1 < NKC) load_x(xf[(i + 1) & 1], kb + i + 1);
-                    compute(ring[i], xf[i & 1]);
-                    if (i + LA < NKC) load_w(ring[i + LA], kb + i + LA);
+                    compute(sring[i % R], xf[i & 1]);
+                    if (i + LA < NKC) load_w(sring[(i + LA) % R], kb + i + LA);
                     // no work of a later unit moves up here, where it would
                     // wait for that unit's loads
                     sched_fence();
@@ -1686,7 +1690,7 @@ void launch_stream_t(const uint16_t* x, const u4_t* pw, const uint16_t* ps, cons
     // activations staged in LDS when all of x fits (one padded slice per wave)
     const size_t xbytes = (size_t)WAVES * stream_slice_bytes(M, K / 128, WAVES);
     if (MT == 1 && xbytes <= kStreamLdsX) {
-        constexpr int D = NPW == 1 ? 16 : 8;
+        constexpr int D = NPW == 1 ? 8 : 4;
         hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D, true>), grid, dim3(64 * WAVES), xbytes, st,
                            x, pw, ps, pz, y, M, N, K, epi);
     } else {
