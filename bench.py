@@ -395,8 +395,8 @@ def ablation(shapes, reps=20):
 def moe(reps=20, sweep=True):
     """Mixtral-8x7B expert FFN on one GPU (512 tokens, top-2 routing over 8
     experts, about 128 rows per expert): the 24 expert GEMMs (w1, w3 over the
-    routed tokens, w2 over fresh [M_e][14336] inputs) as 24 dense launches on
-    pre-gathered activations, against 3 grouped launches that gather the
+    routed tokens, w2 over fresh [M_e][14336] inputs) as 24 dense GEMMs on
+    pre-gathered activations, against 3 grouped GEMMs that gather the
     token rows inside the kernel.  Each form is one HIP graph, checked against
     its eager run and timed with HIP events over `reps` replays (the faster
     of two such timings)."""
@@ -470,10 +470,10 @@ def moe(reps=20, sweep=True):
         return min(e0.elapsed_time(e1) for e0, e1 in evs) / reps * 1e3
 
     t_dense = timed(dense, [m["y_dense"] for m in mats])
-    rows = [dict(form="24 dense launches (pre-gathered rows)", us=round(t_dense, 2),
+    rows = [dict(form="24 dense GEMMs (pre-gathered rows)", us=round(t_dense, 2),
                  tflops=round(flops / t_dense / 1e6, 1))]
     log("Mixtral 8x7B experts, R=%d routed rows (per expert %s), %.1f GFLOP" % (R, counts, flops / 1e9))
-    log("  24 dense launches        %9.2f us  %7.1f TFLOP/s" % (t_dense, flops / t_dense / 1e6))
+    log("  24 dense GEMMs           %9.2f us  %7.1f TFLOP/s" % (t_dense, flops / t_dense / 1e6))
     cfgs = [None]
     if sweep:
         for bm, wn in ((64, 32), (128, 32)):
@@ -482,13 +482,18 @@ def moe(reps=20, sweep=True):
     outs = [m["y_grp"] for m in mats]
     for cfg in cfgs:
         t = timed(lambda: grouped(cfg), outs)
-        name = "auto %s" % (Q.grouped_select_config(R, 8, mats[0]["N"], mats[0]["K"]),) if cfg is None else \
-            "v%d split %d tile %dx%d" % (cfg.variant, cfg.split_k, cfg.tile_m, cfg.tile_n)
+        if cfg is None:
+            sel = Q.grouped_select_config(R, 8, mats[0]["N"], mats[0]["K"])
+            name = "auto %s" % (sel,)
+            if sel["tile_m"] == 128:
+                name += " + remainders < 64 rows in 32x32 tiles"
+        else:
+            name = "v%d split %d tile %dx%d" % (cfg.variant, cfg.split_k, cfg.tile_m, cfg.tile_n)
         diff = max(float((a.float() - b.float()).abs().max() / b.float().abs().max())
                    for a, b in zip(outs, [m["y_dense"] for m in mats]))
-        rows.append(dict(form="3 grouped launches, " + name, us=round(t, 2), tflops=round(flops / t / 1e6, 1),
+        rows.append(dict(form="3 grouped GEMMs, " + name, us=round(t, 2), tflops=round(flops / t / 1e6, 1),
                          speedup=round(t_dense / t, 3), max_rel_diff_vs_dense=round(diff, 6)))
-        log("  3 grouped launches %-40s %9.2f us  %7.1f TFLOP/s  %.2fx  (max rel diff vs dense %.2g)" % (
+        log("  3 grouped GEMMs %-42s %9.2f us  %7.1f TFLOP/s  %.2fx  (max rel diff vs dense %.2g)" % (
             name, t, flops / t / 1e6, t_dense / t, diff))
     # the layer as it runs: w1 and w3 as one grouped launch over their
     # interleaved columns with the gated SiLU fused into the epilogue, then
@@ -508,9 +513,9 @@ def moe(reps=20, sweep=True):
         Q.grouped_gemm(h13, od, *mats[2]["w"], 4096, y=y2)
 
     t = timed(chain, [h13, y2])
-    rows.append(dict(form="2 grouped launches: w1|w3 with the fused gated SiLU, then w2 on its output",
+    rows.append(dict(form="2 grouped GEMMs: w1|w3 with the fused gated SiLU, then w2 on its output",
                      us=round(t, 2), tflops=round(flops / t / 1e6, 1), speedup=round(t_dense / t, 3)))
-    log("  2 grouped launches, fused SiLU gate    %9.2f us  %7.1f TFLOP/s  %.2fx" % (t, flops / t / 1e6, t_dense / t))
+    log("  2 grouped GEMMs, fused SiLU gate       %9.2f us  %7.1f TFLOP/s  %.2fx" % (t, flops / t / 1e6, t_dense / t))
     return dict(routed_rows=R, rows_per_expert=counts, gflop=round(flops / 1e9, 2), rows=rows)
 
 
@@ -559,7 +564,7 @@ def main():
     ap.add_argument("--configs", default="2,5", help="workload configs (2 = Llama-2-7B, 5 = Llama-2-70B)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--moe", action="store_true",
-                    help="time the Mixtral-8x7B expert GEMMs: 24 dense launches vs 3 grouped launches")
+                    help="time the Mixtral-8x7B expert GEMMs: 24 dense GEMMs vs 3 grouped GEMMs")
     ap.add_argument("--moe-auto-only", action="store_true", help="with --moe: only the automatic grouped config")
     ap.add_argument("--cpu-col-fraction", type=float, default=1.0 / 8)
     ap.add_argument("--points-out", default="", help="optional path for the per-GEMM table (JSON)")

@@ -50,7 +50,11 @@ extern "C" {
  *            K % 128 == 0); group must be 128
  * R == 0 is a valid no-op.  Asynchronous on `stream` (hipStream_t as void*,
  * NULL = default stream); the library's internal workspace is used as by
- * quick_w4a16_gemm.  rows and offsets are read on the device only: values
+ * quick_w4a16_gemm.  When the automatic choice takes 128-row tiles (about
+ * 96 or more routed rows per expert), the GEMM runs as two launches on
+ * `stream`: each expert's whole 128-row tiles, and a remainder of at least
+ * 64 rows, with those tiles; then the shorter remainders with 32-row tiles,
+ * so that a remainder of a few rows does not pay for a full-height tile.  rows and offsets are read on the device only: values
  * that break the contract above (out-of-range tokens or offsets,
  * decreasing offsets) are clamped into range, so the kernel stays inside
  * every buffer, but the affected rows of y are then unspecified.
@@ -66,19 +70,23 @@ int quick_w4a16_grouped_gemm(const void* x, const int32_t* rows, const int32_t* 
  * workspace contract as quick_w4a16_gemm_ex).  cfg: variant 0 = automatic,
  * 2 = one workgroup per (tile, K slice) with split_k K slices (0 = 1),
  * 3 = stream-K over split_k resident workgroups (a multiple of 8, 0 = all
- * resident); (tile_m, tile_n) one of (16, 16), (32, 16), (64, 32),
- * (128, 32), 0 = automatic; variant 1 (the stream kernel) is not available
- * here (INVALID_ARG). */
+ * resident); (tile_m, tile_n) one of (16, 16), (16, 32), (32, 16),
+ * (32, 32), (64, 32), (128, 32), 0 = automatic; variant 1 (the stream
+ * kernel) is not available here (INVALID_ARG).  A cfg with every field 0
+ * is the automatic choice (including its two-launch form); any other cfg
+ * runs as one launch. */
 int quick_w4a16_grouped_gemm_ex(const void* x, const int32_t* rows, const int32_t* offsets, const void* packed,
                                 const void* scales, const void* zeros, void* y, int64_t T, int64_t R, int64_t E,
                                 int64_t N, int64_t K, int64_t group, void* stream, const quick_config_t* cfg,
                                 void* workspace, size_t workspace_bytes);
 
 /* Workspace bytes quick_w4a16_grouped_gemm_ex needs (cfg NULL = automatic
- * choice); 0 when none, or for invalid arguments. */
+ * choice; for its two-launch form, the larger of the two launches' needs);
+ * 0 when none, or for invalid arguments. */
 size_t quick_grouped_workspace_bytes(int64_t R, int64_t E, int64_t N, int64_t K, const quick_config_t* cfg);
 
-/* The automatic choice for R routed rows over E experts.
+/* The automatic choice for R routed rows over E experts (for the two-launch
+ * form, the first launch's configuration).
  * Errors: INVALID_ARG (NULL cfg), SHAPE. */
 int quick_grouped_select_config(int64_t R, int64_t E, int64_t N, int64_t K, quick_config_t* cfg);
 

@@ -253,16 +253,20 @@ __device__ __forceinline__ uint32_t ld16(rsrc_t r, uint32_t voff, uint32_t soff)
 // WAVES waves split the k-groups between them (in-workgroup split-K, no
 // partial sums leave the workgroup).  Each wave streams its packed units from
 // HBM with one 16-byte load per lane and unit through a ring of D register
-// stages, so D k-groups of weights are in flight while one is dequantized and
-// multiplied.  At the end the waves' fp32 partial tiles are summed through
-// LDS in wave order (deterministic) and stored.
+// stages, so D-1 k-groups of weights are in flight while one is dequantized
+// and multiplied; a short k-range (activations in LDS) instead runs as one
+// pass specialised on its unit count with a few units requested ahead.  At
+// the end the waves' fp32 partial tiles are summed through LDS in wave order
+// (deterministic) and stored.
 //
 // Activation fragments (B operand, MT blocks of 16 rows):
 //  * XL: the wave first copies its own k-range of all M rows of x into its
 //    slice of LDS with the 16-byte LDS-DMA load (rows contiguous, row stride
-//    = the slice width), waits for it, and then reads fragments with LDS
-//    reads; lanes of rows >= M read row M-1 (broadcast).  No barrier: a wave
-//    only reads what it copied.  Used when all of x fits (M*K*2 bytes).
+//    = the slice width), waits for it (the copy is issued before the weight
+//    loads, so the wait lets those stay in flight), and then reads fragments
+//    with LDS reads; lanes of rows >= M read row M-1 (broadcast).  No
+//    barrier: a wave only reads what it copied.  Used when all waves' slices
+//    fit in 64 KiB.
 //  * otherwise the fragments are 16-byte buffer loads from global memory
 //    (they are small and shared by every workgroup, so they hit in cache),
 //    one k-group ahead.
@@ -609,6 +613,13 @@ struct GroupArgs {
     const int* offsets;  // [experts + 1] first routed row of each expert
     int experts;
     int routed;          // rows of y
+    // Which of each expert's rows this launch covers.  0: all.  With
+    // `unit` rows per full tile: 1 = the leading whole tiles, plus the
+    // remainder when it holds at least `keep` rows; 2 = the rest (a
+    // remainder of fewer than `keep` rows), for a launch with shorter tiles.
+    int part;
+    int unit;
+    int keep;
 };
 
 // WB != 0 builds the write-back ablation of the conventional design (the
@@ -687,6 +698,12 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
                 if (e < ga.experts) {
                     lo = min(max(ga.offsets[e], 0), ga.routed);
                     hi = min(max(ga.offsets[e + 1], lo), ga.routed);
+                    if (ga.part) {
+                        const int rem = (hi - lo) % ga.unit;
+                        const int lead = rem >= ga.keep ? hi : hi - rem;   // end of part 1
+                        if (ga.part == 1) hi = lead;
+                        else lo = lead;
+                    }
                 }
                 int t = (hi - lo + BM - 1) / BM;
 #pragma unroll
@@ -2265,6 +2282,22 @@ size_t grouped_workspace(int64_t R, int64_t N, const Plan& pl)
     return 0;
 }
 
+// The automatic grouped plan with full-height (128-row) tiles runs in two
+// launches: the experts' whole tiles (and remainders of at least 64 rows)
+// with the 128-row tiles, then the short remainders with 32-row tiles, so a
+// remainder of a few rows does not cost a full-height tile's matrix work.
+// Returns whether `pl` is split that way, and the second launch's plan.
+constexpr int kGroupTileUnit = 128;
+constexpr int kGroupTailKeep = 64;
+bool grouped_tail_plan(int64_t R, int64_t E, int64_t N, int64_t K, const quick_config_t* cfg, const Plan& pl,
+                       Plan* tp)
+{
+    const bool automatic = !cfg || (cfg->variant == 0 && cfg->split_k == 0 && cfg->tile_m == 0 && cfg->tile_n == 0);
+    if (!automatic || pl.bm != kGroupTileUnit) return false;
+    const quick_config_t tc{kVariantStreamK, 0, 32, 32};
+    return grouped_plan(R, E, N, K, &tc, tp) == QUICK_OK;
+}
+
 // The epilogue's constraints on a grouped plan (see epilogue_plan).
 int grouped_epilogue_plan(const Epi& epi, const quick_config_t* cfg, Plan* pl)
 {
@@ -2294,9 +2327,11 @@ int grouped_impl(const void* x, const int32_t* rows, const int32_t* offsets, con
     if (st) return st;
     st = grouped_epilogue_plan(epi, cfg, &pl);
     if (st) return st;
+    Plan tp;
+    const bool tail = grouped_tail_plan(R, E, N, K, cfg, pl, &tp);
     if (R == 0) return QUICK_OK;
     hipStream_t hs = (hipStream_t)stream;
-    const size_t need = grouped_workspace(R, N, pl);
+    const size_t need = std::max(grouped_workspace(R, N, pl), tail ? grouped_workspace(R, N, tp) : 0);
     void* ws = nullptr;
     if (need) {
         if (workspace) {
@@ -2308,12 +2343,17 @@ int grouped_impl(const void* x, const int32_t* rows, const int32_t* offsets, con
             if (st) return st;
         }
     }
-    const GroupArgs ga{rows, offsets, (int)E, (int)R};
     (void)hipGetLastError();
-    st = launch_tiled(pl, static_cast<const uint16_t*>(x), static_cast<const u4_t*>(packed),
-                      static_cast<const uint16_t*>(scales), static_cast<const uint32_t*>(zeros),
-                      static_cast<uint16_t*>(y), static_cast<float*>(ws), (int)T, (int)N, (int)K, hs, epi, &ga);
-    if (st) return st;
+    // the two launches write disjoint rows of y; the second reuses the
+    // workspace after the first (same stream; stream-K leaves its counters
+    // zero)
+    for (int part = tail ? 1 : 0; part <= (tail ? 2 : 0); ++part) {
+        const GroupArgs ga{rows, offsets, (int)E, (int)R, part, kGroupTileUnit, kGroupTailKeep};
+        st = launch_tiled(part == 2 ? tp : pl, static_cast<const uint16_t*>(x), static_cast<const u4_t*>(packed),
+                          static_cast<const uint16_t*>(scales), static_cast<const uint32_t*>(zeros),
+                          static_cast<uint16_t*>(y), static_cast<float*>(ws), (int)T, (int)N, (int)K, hs, epi, &ga);
+        if (st) return st;
+    }
     return hipGetLastError() == hipSuccess ? QUICK_OK : QUICK_ERR_HIP;
 }
 
@@ -2342,9 +2382,10 @@ extern "C" size_t quick_grouped_workspace_bytes(int64_t R, int64_t E, int64_t N,
                                                 const quick_config_t* cfg)
 {
     if (R <= 0 || E < 1 || E > kMaxExperts || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return 0;
-    Plan pl;
+    Plan pl, tp;
     if (grouped_plan(R, E, N, K, cfg, &pl)) return 0;
-    return grouped_workspace(R, N, pl);
+    const bool tail = grouped_tail_plan(R, E, N, K, cfg, pl, &tp);
+    return std::max(grouped_workspace(R, N, pl), tail ? grouped_workspace(R, N, tp) : 0);
 }
 
 extern "C" int quick_grouped_select_config(int64_t R, int64_t E, int64_t N, int64_t K, quick_config_t* cfg)
@@ -2408,10 +2449,11 @@ extern "C" size_t quick_grouped_fused_workspace_bytes(int64_t R, int64_t E, int6
                                                       const quick_config_t* cfg, const quick_epilogue_t* epi)
 {
     if (R <= 0 || E < 1 || E > kMaxExperts || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return 0;
-    Plan pl;
+    Plan pl, tp;
     if (grouped_plan(R, E, N, K, cfg, &pl)) return 0;
     if (grouped_epilogue_plan(to_epi(epi), cfg, &pl)) return 0;
-    return grouped_workspace(R, N, pl);
+    const bool tail = grouped_tail_plan(R, E, N, K, cfg, pl, &tp);
+    return std::max(grouped_workspace(R, N, pl), tail ? grouped_workspace(R, N, tp) : 0);
 }
 
 extern "C" int quick_interleave_gate_up(const uint8_t* q_gate, const uint8_t* z_gate, const uint16_t* s_gate,

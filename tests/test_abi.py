@@ -184,6 +184,14 @@ def test_grouped_validation_without_device():
     assert Q.grouped_workspace_bytes(1024, 8, 14336, 4096, cfg) == Q.WS_COUNTER_BYTES + 2 * 64 * 128 * 256 * 4
     assert Q.grouped_workspace_bytes(1024, 8, 14336, 4096, Q.make_config(variant=2, tile_m=16, tile_n=16)) == 0
     assert Q.grouped_workspace_bytes(0, 8, 14336, 4096) == 0
+    # the automatic full-height plan runs two stream-K launches (128-row tiles,
+    # then 32-row tiles over short remainders): its workspace covers both, and
+    # an all-zero cfg is the automatic choice
+    main = Q.grouped_workspace_bytes(1024, 8, 14336, 4096, Q.make_config(variant=3, tile_m=128, tile_n=32))
+    tail = Q.grouped_workspace_bytes(1024, 8, 14336, 4096, Q.make_config(variant=3, tile_m=32, tile_n=32))
+    auto = Q.grouped_workspace_bytes(1024, 8, 14336, 4096)
+    assert auto == max(main, tail) > 0
+    assert Q.grouped_workspace_bytes(1024, 8, 14336, 4096, Q.make_config()) == auto
 
 
 def test_fused_validation_without_device():

@@ -122,3 +122,31 @@ def test_grouped_gated_with_expert_bias():
                 continue
             ref = oracle.epilogue(oracle.gemm(x[rows[lo:hi]], *experts[e]), bias[e] if with_bias else None, act=1)
             assert rel_err(y[lo:hi], ref) <= TOL, "expert %d" % e
+
+
+def test_grouped_gated_auto_two_parts():
+    """Per-expert bias and the gated SiLU through the automatic two-launch
+    plan (about 128 rows per expert: 128-row tiles, then 32-row tiles over
+    the short remainders)."""
+    T, K, Nh = 300, 512, 128
+    counts = [131, 0, 127, 150, 100]
+    E = len(counts)
+    experts = [_gate_up(90 + e, K, Nh) for e in range(E)]
+    N = 2 * Nh
+    x = rand_case(91, T, K, 16)[0]
+    g = np.random.Generator(np.random.PCG64(92))
+    rows = np.concatenate([np.sort(g.integers(0, T, c)) for c in counts]).astype(np.int32)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    bias = np.stack([_bias(93 + e, N) for e in range(E)])
+    assert Q.grouped_select_config(int(offsets[-1]), E, N, K)["tile_m"] == 128
+    dw, ds, dz = Q.to_device(*Q.pack_experts(experts))
+    say("grouped gated two parts")
+    y = from_dev_y(Q.grouped_gemm_fused(to_dev_x(x), torch.from_numpy(offsets).cuda(), dw, ds, dz, N,
+                                        rows=torch.from_numpy(rows).cuda(), bias=_dev_bias(bias.reshape(-1)),
+                                        activation=Q.ACT_SILU_GATE))
+    for e in range(E):
+        lo, hi = offsets[e], offsets[e + 1]
+        if hi == lo:
+            continue
+        ref = oracle.epilogue(oracle.gemm(x[rows[lo:hi]], *experts[e]), bias[e], act=1)
+        assert rel_err(y[lo:hi], ref) <= TOL, "expert %d" % e

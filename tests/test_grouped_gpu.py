@@ -148,6 +148,31 @@ def test_grouped_streamk_deterministic_and_caller_workspace():
     assert rel_err(y0, oracle.grouped_gemm(x, rows, offsets, experts)) <= TOL
 
 
+@pytest.mark.parametrize("counts", [[130, 149, 111, 20, 257, 0, 128, 200], [129, 131, 127, 128]])
+def test_grouped_auto_full_height_two_parts(counts):
+    """The automatic plan for about 128 rows per expert runs as two launches
+    (128-row tiles over whole tiles and remainders of >= 64 rows, then 32-row
+    tiles over the short remainders): every row against the oracle, the
+    workspace query covering both launches, repeated calls identical."""
+    T, K, N = 400, 512, 256
+    E = len(counts)
+    experts = _experts(81, E, K, N)
+    x, _, _, _ = rand_case(82, T, K, 16)
+    rows, offsets = _routing(83, T, E, counts=counts)
+    R = int(offsets[-1])
+    assert Q.grouped_select_config(R, E, N, K)["tile_m"] == 128
+    G = Grouped(experts)
+    xd = to_dev_x(x)
+    say("grouped two parts R=%d counts=%s" % (R, counts))
+    y0 = from_dev_y(G.run(xd, rows, offsets))
+    nb = Q.grouped_workspace_bytes(R, E, N, K)
+    ws = torch.zeros(nb // 4 + 1, dtype=torch.int32, device="cuda")
+    y1 = from_dev_y(G.run(xd, rows, offsets, workspace=ws))
+    assert np.array_equal(y0, y1)
+    assert int(ws[:Q.WS_COUNTER_BYTES // 4].abs().sum().item()) == 0
+    assert rel_err(y0, oracle.grouped_gemm(x, rows, offsets, experts)) <= TOL
+
+
 def test_grouped_zero_rows_is_noop():
     experts = _experts(51, 2, 128, 16)
     G = Grouped(experts)

@@ -79,14 +79,22 @@ def test_streamk_contributors_and_slots(tiles, KG, G):
             assert slot == 2 * wid + (0 if wid * U // G >= tb else 1)
 
 
-def grouped_tiles(offsets, R, BM, nn):
-    """The grouped kernel's tile table (clamped offsets, per-expert m-tile
-    counts, prefix sums) and its tile -> (expert, m0, mend, n-tile) map."""
+def grouped_tiles(offsets, R, BM, nn, part=0, unit=128, keep=64):
+    """The grouped kernel's tile table (clamped offsets, the rows of this
+    launch's part, per-expert m-tile counts, prefix sums) and its tile ->
+    (expert, m0, mend, n-tile) map."""
     E = len(offsets) - 1
     lo, hi, cum = [], [], [0]
     for e in range(E):
         a = min(max(offsets[e], 0), R)
         b = min(max(offsets[e + 1], a), R)
+        if part:
+            rem = (b - a) % unit
+            lead = b if rem >= keep else b - rem
+            if part == 1:
+                b = lead
+            else:
+                a = lead
         lo.append(a), hi.append(b), cum.append(cum[-1] + (b - a + BM - 1) // BM)
 
     def tile(t):
@@ -120,6 +128,31 @@ def test_grouped_tile_table_covers_every_row_once(counts, BM):
         assert offsets[e] <= m0 < mend <= offsets[e + 1] and nt < nn
         seen[m0:min(m0 + BM, mend), nt] += 1
     assert np.all(seen == 1)
+
+
+@pytest.mark.parametrize("counts", [[130, 149, 111, 127, 132, 133, 122, 120], [20, 0, 257, 128, 200, 63, 64, 1],
+                                    [0, 0, 0], [300], [127, 129, 191, 192, 193]])
+def test_grouped_two_part_split_covers_every_row_once(counts):
+    """The automatic full-height grouped plan runs as two launches: 128-row
+    tiles over each expert's whole tiles (and a remainder of >= 64 rows),
+    then 32-row tiles over the short remainders.  Together they cover every
+    routed row once; the second part holds fewer than 64 rows per expert."""
+    offsets = np.concatenate([[0], np.cumsum(counts)]).tolist()
+    R = offsets[-1]
+    nn = 2
+    seen = np.zeros((max(R, 1), nn), np.int64)
+    for part, BM in ((1, 128), (2, 32)):
+        n_mt, tile = grouped_tiles(offsets, R, BM, nn, part=part)
+        per_expert = {}
+        for t in range(n_mt * nn):
+            e, m0, mend, nt = tile(t)
+            assert offsets[e] <= m0 < mend <= offsets[e + 1]
+            rows = min(m0 + BM, mend) - m0
+            seen[m0:m0 + rows, nt] += 1
+            per_expert[e] = per_expert.get(e, 0) + rows
+        if part == 2:
+            assert all(v < 2 * 64 for v in per_expert.values())     # nn n-tiles x < 64 rows
+    assert np.all(seen[:R] == 1)
 
 
 def test_grouped_tile_table_clamps_malformed_offsets():
