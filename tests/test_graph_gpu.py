@@ -1,7 +1,8 @@
 """GEMMs captured in a HIP graph replay the eager results bit for bit.
 
 Every kernel path (stream kernel, tiled data-parallel, split-K with its
-reduction kernel, stream-K with its arrival counters) is captured after an
+reduction kernel, stream-K with its arrival counters; the grouped GEMM's
+two-launch plan and a fused epilogue) is captured after an
 eager warm-up on the capture stream (so the library's per-stream workspace
 exists and the capture allocates nothing).  The graph is replayed several
 times with unrelated eager work and synchronizations in between, and every
@@ -59,4 +60,53 @@ def test_graph_replay_matches_eager():
             assert torch.equal(y, eager[i]), "replay %d differs from eager for case %d" % (rep, i)
         # unrelated eager work between replays (same library, default stream)
         other.gemm(to_dev_x(other_x), cfg=Q.make_config(variant=2, tile_m=32, tile_n=16, split_k=4))
+        torch.cuda.synchronize()
+
+
+def test_graph_replay_grouped_and_fused():
+    """The grouped GEMM's automatic two-launch plan (128-row tiles, then
+    32-row tiles over short remainders, both stream-K) and a fused gated
+    epilogue, captured together after an eager warm-up and replayed with
+    eager work in between: every replay equals the eager outputs."""
+    side = torch.cuda.Stream()
+    g_np = np.random.Generator(np.random.PCG64(41))
+    T, K, N, E = 300, 512, 256, 4
+    experts = []
+    for _ in range(E):
+        experts.append((g_np.integers(0, 16, (K, N), dtype=np.uint8),
+                        g_np.integers(0, 16, (K // 128, N), dtype=np.uint8),
+                        g_np.uniform(0.002, 0.02, (K // 128, N)).astype(np.float16).view(np.uint16)))
+    counts = [131, 149, 100, 128]
+    rows = torch.from_numpy(np.concatenate([np.sort(g_np.integers(0, T, c)) for c in counts]).astype(np.int32)).cuda()
+    offsets = torch.from_numpy(np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)).cuda()
+    R = int(sum(counts))
+    assert Q.grouped_select_config(R, E, N, K)["tile_m"] == 128
+    dw, ds, dz = Q.to_device(*Q.pack_experts(experts))
+    x = to_dev_x(rand_case(42, T, K, 16)[0])
+    yg = torch.empty((R, N), dtype=torch.float16, device="cuda")
+    xf, qf, zf, sf = rand_case(43, 40, 640, 96)
+    pf = Packed(qf, zf, sf)
+    xfd = to_dev_x(xf)
+    yf = torch.empty((40, 48), dtype=torch.float16, device="cuda")
+
+    def run_all():
+        Q.grouped_gemm(x, offsets, dw, ds, dz, N, rows=rows, y=yg)
+        Q.gemm_fused(xfd, pf.dw, pf.ds, pf.dz, 96, activation=Q.ACT_SILU_GATE, y=yf)
+
+    with torch.cuda.stream(side):
+        run_all()
+    side.synchronize()
+    eager = [yg.clone(), yf.clone()]
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=side):
+        run_all()
+    for rep in range(3):
+        yg.fill_(float("nan"))
+        yf.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(yg, eager[0]) and torch.equal(yf, eager[1]), "replay %d differs" % rep
+        Q.grouped_gemm(x, offsets, dw, ds, dz, N, rows=rows, cfg=Q.make_config(variant=2, split_k=2, tile_m=32,
+                                                                               tile_n=16))
         torch.cuda.synchronize()
