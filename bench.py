@@ -49,6 +49,10 @@ def log(*a):
 def kernel_name(sel: dict) -> str:
     if sel["variant"] == 1:
         return "stream_kernel<MT,%d,%d>" % (sel["tile_n"], sel["split_k"])
+    if sel["variant"] == 4:
+        return "bstream_kernel(G=%d)" % sel["split_k"]
+    if sel["variant"] == 5:
+        return "kstream_kernel<%d>(S=%d)" % (sel["tile_n"], sel["split_k"])
     name = "tiled_kernel<%d,%d>" % (sel["tile_m"], sel["tile_n"])
     if sel["variant"] == 3:
         name += "+streamK(G=%d)" % sel["split_k"]

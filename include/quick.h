@@ -116,19 +116,25 @@ typedef struct quick_config {
                       4 = balanced stream kernel (M <= 16, M*K*2 bytes
                       <= 128 KiB and K a multiple of 2048: every wave of the
                       chip streams an equal share of the 16 x 128 weight
-                      units)                                                 */
+                      units),
+                      5 = sliced stream kernel (M <= 16: the 8 waves of a
+                      workgroup split 128 or 256 columns, workgroups split
+                      K into slices of at most 2048 channels whose rows of x
+                      they stage in LDS once; N/128 <= 4096)                */
     int split_k;   /* variant 2: K slices across workgroups; variant 1: waves
                       per workgroup (1, 2, 4, 8); variant 3: resident
                       workgroups, a multiple of 8 up to 4096 (clamped to the
                       number of tile x 128-channel units); variant 4:
                       workgroups of 8 waves, up to 512 (0 = one per compute
-                      unit); 0 = auto                                        */
+                      unit); variant 5: K slices (raised to at least
+                      ceil(K/2048), at most K/128); 0 = auto                */
     int tile_m;    /* tiled kernel rows per workgroup: 16, 32, 64 or 128
-                      (variant 4: must be 0, as tile_n);
+                      (variants 4 and 5: must be 0; variant 4: tile_n too);
                       supported (tile_m, tile_n) pairs: (16|32, 16|32),
                       (64, 32), (64, 64), (128, 32)                         */
     int tile_n;    /* tiled kernel columns per wave: 16, 32 or 64
-                      stream kernel: n-tiles per wave: 1 or 2                 */
+                      stream kernels (variants 1, 5): n-tiles per wave: 1 or
+                      2                                                      */
 } quick_config_t;
 
 /* Leading bytes of a workspace that hold stream-K arrival counters. */

@@ -46,6 +46,7 @@ VARIANT_STREAM = 1
 VARIANT_TILED = 2
 VARIANT_STREAMK = 3
 VARIANT_BSTREAM = 4
+VARIANT_KSTREAM = 5
 
 # leading workspace bytes that hold stream-K arrival counters (QUICK_WORKSPACE_COUNTER_BYTES)
 WS_COUNTER_BYTES = 16384

@@ -1333,6 +1333,200 @@ bstream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     }
 }
 
+// ---------------------------------------------------------------------------
+// Sliced stream kernel (M <= 16, bandwidth-bound).
+//
+// The stream kernel gives a workgroup a few n-tiles and the whole K, so every
+// workgroup reads all of x: at M = 16 that is 2 (two n-tiles per wave) to 4
+// bytes of activations from L2 per byte of packed weights, and once 16 rows
+// of K channels outgrow its LDS they come as global loads.  Here the 8 waves
+// of a workgroup split the columns instead (wave w streams n-tiles
+// 8*NPW*cg + NPW*w .. +NPW-1 of column group cg) and the workgroups split K
+// into S slices of at most 16 k-groups.  A workgroup copies its slice of x
+// (M rows x its k-groups) into LDS once with the 16-byte LDS-DMA load, and all
+// 8 waves read their fragments from there, so activations cost 1/(2 NPW)
+// byte per weight byte.  Inside a 256-byte piece of the slice (one row, one
+// k-group) the 16-byte chunk with channels 8q .. 8q+7 sits at position
+// q ^ (row % 16), so the 16 rows of a fragment read hit distinct banks.  Each
+// wave then runs the stream kernel's single pass over its units: specialised
+// on the unit count, a few units requested ahead, every unit multiplied as it
+// lands; weights are loaded and dequantized straight into VGPRs as in the
+// other kernels.
+//
+// With S > 1 each workgroup writes its fp32 partial columns with
+// device-coherent stores and bumps its column group's arrival counter; the
+// last of the S to arrive adds the partials in slice order (so the result
+// does not depend on who is last), applies the epilogue, rounds once, stores
+// y and re-arms the counter.  Workgroup ids map onto (slice, column group)
+// slice-major with consecutive ids on one XCD, so the workgroups of an XCD
+// share one activation slice in its L2.
+// ---------------------------------------------------------------------------
+constexpr int kKsWaves = 8;
+constexpr int kKsMaxKg = kStreamSinglePass;   // k-groups per slice
+constexpr size_t kKsLds = 64 * 1024;          // LDS bytes for the slice (16 rows x 16 k-groups)
+
+template <int NPW>
+__global__ void __launch_bounds__(64 * kKsWaves)
+kstream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
+               const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
+               uint16_t* __restrict__ y, float* __restrict__ ws, int M, int N, int K,
+               int kgps, int n_cg, int S, Epi epi)
+{
+    extern __shared__ __attribute__((aligned(1024))) uint8_t xs[];
+    __shared__ int ks_last;
+    const int KG = K >> 7;
+    const int NT = N >> 4;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int c = lane & 15;
+    const int g = lane >> 4;
+    // gridDim.x is a multiple of 8; ids past the n_cg * S workgroups exit
+    const int t = (blockIdx.x & 7) * (gridDim.x >> 3) + (blockIdx.x >> 3);
+    if (t >= n_cg * S) return;
+    const int s = t / n_cg;
+    const int cg = t - s * n_cg;
+    const int kb = s * kgps;
+    const int nk = min(KG, kb + kgps) - kb;   // 1 .. 16: the host leaves no slice empty
+    const int ntw = cg * (kKsWaves * NPW) + wave * NPW;
+
+    const rsrc_t rw = make_rsrc(pw, (uint32_t)((size_t)K * N / 2));
+    const rsrc_t rs = make_rsrc(ps, (uint32_t)((size_t)K * N / 64));
+    const rsrc_t rz = make_rsrc(pz, (uint32_t)((size_t)K * N / 256));
+    const rsrc_t rx = make_rsrc(x, (uint32_t)((size_t)M * K * 2));
+    // n-tiles past the end are clamped to the last one: computed on valid
+    // data, never stored
+    uint32_t ubase[NPW];
+#pragma unroll
+    for (int p = 0; p < NPW; ++p) ubase[p] = (uint32_t)min(ntw + p, NT - 1) * KG;
+    const uint32_t vw = lane * 16;
+    const uint32_t vs = c * 2;
+    const uint32_t vz = (c >> 3) * 4;
+
+    // Copy the slice: LDS chunk i (16 bytes) is row i / (16 nk), chunk
+    // position q = i % (16 nk) of that row's slice, holding source chunk
+    // (q & ~15) | ((q ^ row) & 15).  Instruction i0 / 64 moves chunks
+    // i0 .. i0+63; lanes past the last chunk re-read it into the padding of
+    // the allocation (whole KiB).
+    const int chunks = M * nk * 16;
+    for (int i0 = wave * 64; i0 < chunks; i0 += 64 * kKsWaves) {
+        const int idx = min(i0 + lane, chunks - 1);
+        const int row = idx / (nk * 16);
+        const int q = idx - row * nk * 16;
+        const int qs = (q & ~15) | ((q ^ row) & 15);
+        dma16(rx, xs + (size_t)i0 * 16, (uint32_t)(row * K + kb * 128 + qs * 8) * 2, 0);
+    }
+
+    // fragment of step j: row c (rows past M read row M-1), channels
+    // 32j + 8g .. +7 of the k-group
+    const int row = min(c, M - 1);
+    uint32_t xq[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) xq[j] = (uint32_t)(row * nk * 256) + ((((4 * j + g) ^ row) & 15) << 4);
+    auto load_x = [&](u4_t (&xb)[4], int kl) __attribute__((always_inline)) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) xb[j] = *reinterpret_cast<const u4_t*>(xs + xq[j] + kl * 256);
+    };
+    auto load_w = [&](WStage<NPW>& st, int kg) __attribute__((always_inline)) {
+#pragma unroll
+        for (int p = 0; p < NPW; ++p) {
+            const uint32_t u = uniform(ubase[p] + kg);
+            st.w[p] = ld128(rw, vw, u * 1024u);
+            st.s[p] = ld16(rs, vs, u * 32u);
+            st.z[p] = ld32(rz, vz, u * 8u);
+        }
+    };
+    f4_t acc[NPW];
+#pragma unroll
+    for (int p = 0; p < NPW; ++p) acc[p] = f4_t{0.f, 0.f, 0.f, 0.f};
+    auto compute = [&](const WStage<NPW>& st, const u4_t (&xb)[4]) __attribute__((always_inline)) {
+        Deq d[NPW];
+#pragma unroll
+        for (int p = 0; p < NPW; ++p) d[p] = make_deq(st.s[p], (st.z[p] >> (4 * (c & 7))) & 15u);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int p = 0; p < NPW; ++p) acc[p] = mfma16(dequant8(st.w[p][j], d[p]), bits_as<h8_t>(xb[j]), acc[p]);
+    };
+
+    u4_t xf[2][4];
+    with_count<kKsMaxKg>(nk, [&](auto nkc) {
+        constexpr int NKC = decltype(nkc)::value;
+        constexpr int LA = NKC < kStreamLookahead ? NKC : kStreamLookahead;
+        constexpr int R = LA + 1;
+        WStage<NPW> sring[R];
+#pragma unroll
+        for (int i = 0; i < LA; ++i) {
+            load_w(sring[i], kb + i);
+            sched_fence();
+        }
+        if constexpr (NKC > 0) {
+            // this wave's copy instructions, issued before these 3 * NPW * LA
+            // loads, have landed; after the barrier every wave's have (all
+            // waves of the workgroup have the same unit count)
+            wait_vm<3 * NPW * LA>();
+            barrier();
+            asm volatile("" ::: "memory");
+            sched_fence();
+            load_x(xf[0], 0);
+#pragma unroll
+            for (int i = 0; i < NKC; ++i) {
+                if (i + 1 < NKC) load_x(xf[(i + 1) & 1], i + 1);
+                compute(sring[i % R], xf[i & 1]);
+                if (i + LA < NKC) load_w(sring[(i + LA) % R], kb + i + LA);
+                sched_fence();
+            }
+        }
+    });
+
+    // row c, columns 16 * (ntw + p) + 4g .. +3 (gated form: NPW == 2 and ntw
+    // even, so tile 0 is a gate tile and tile 1 its up tile)
+    auto store = [&](const f4_t (&v)[NPW]) __attribute__((always_inline)) {
+        if (c >= M) return;
+        if (NPW == 2 && epi.act) {
+            if (ntw < NT) store_gated(y, epi, c, N, ntw * 16 + 4 * g, v[0], v[NPW - 1]);
+            return;
+        }
+#pragma unroll
+        for (int p = 0; p < NPW; ++p)
+            if (ntw + p < NT) store_out(y, epi, c, N, (ntw + p) * 16 + 4 * g, v[p]);
+    };
+    if (S == 1) {
+        store(acc);
+        return;
+    }
+    // partials: slot (cg, slice) holds the workgroup's 8 * NPW tiles, 1 KiB each
+    constexpr uint32_t WG_BYTES = kKsWaves * NPW * 1024;
+    unsigned* counters = reinterpret_cast<unsigned*>(ws);
+    const rsrc_t rp = make_rsrc(ws + kSkCounterBytes / sizeof(float), (uint32_t)n_cg * S * WG_BYTES);
+    auto slot = [&](int ss, int p) {
+        return uniform((uint32_t)(cg * S + ss) * WG_BYTES + (uint32_t)(wave * NPW + p) * 1024u);
+    };
+#pragma unroll
+    for (int p = 0; p < NPW; ++p)
+        __builtin_amdgcn_raw_buffer_store_b128(bits_as<u4_t>(acc[p]), rp, lane * 16u, slot(s, p), kCoherentAux);
+    wait_all();       // this wave's partials are written through
+    __syncthreads();  // ... and every wave's
+    if (threadIdx.x == 0)
+        ks_last = __hip_atomic_fetch_add(&counters[cg], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                  (unsigned)(S - 1);
+    __syncthreads();
+    if (!ks_last) return;
+    f4_t tot[NPW];
+#pragma unroll
+    for (int p = 0; p < NPW; ++p) {
+        f4_t sum = f4_t{0.f, 0.f, 0.f, 0.f};
+        for (int ss = 0; ss < S; ++ss) {
+            const f4_t v = ss == s ? acc[p]
+                                   : bits_as<f4_t>(__builtin_amdgcn_raw_buffer_load_b128(rp, lane * 16u, slot(ss, p),
+                                                                                        kCoherentAux));
+            sum = ss == 0 ? v : sum + v;
+        }
+        tot[p] = sum;
+    }
+    store(tot);
+    if (threadIdx.x == 0) __hip_atomic_store(&counters[cg], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Sum of S fp32 partial outputs [S][rows][N] in split order, then the
 // epilogue and one rounding to f16.  One thread per 4 output columns.
 __global__ void __launch_bounds__(256)
@@ -1366,6 +1560,7 @@ constexpr size_t kStreamLdsX = 64 * 1024;  // LDS bytes the stream kernel may gi
 constexpr int kVariantTiled = 2;
 constexpr int kVariantStreamK = 3;  // tiled kernel, stream-K schedule
 constexpr int kVariantBStream = 4;  // balanced stream kernel
+constexpr int kVariantKStream = 5;  // sliced stream kernel
 constexpr size_t kBStreamLdsX = 128 * 1024;  // LDS bytes the balanced stream kernel may give to x
 constexpr int kBStreamDepth = 16;            // its register ring depth (units in flight per wave)
 
@@ -1400,6 +1595,11 @@ struct Plan {
 };
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
+
+// Column groups (8 waves x npw n-tiles) of the sliced stream kernel, and the
+// fewest K slices that keep each slice within its 16 k-groups.
+int ks_groups(int64_t N, int npw) { return ceil_div(N / 16, kKsWaves * npw); }
+int ks_min_slices(int64_t K) { return ceil_div(K / 128, kKsMaxKg); }
 
 bool is_tiled(int variant) { return variant == kVariantTiled || variant == kVariantStreamK; }
 
@@ -1556,7 +1756,21 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
     if (!cfg && tuned_config(M, N, K, &tuned)) cfg = &tuned;
     if (!cfg) return QUICK_OK;
     const int64_t KG = K / 128;
-    if (cfg->variant < 0 || cfg->variant > 4 || cfg->split_k < 0) return QUICK_ERR_INVALID_ARG;
+    if (cfg->variant < 0 || cfg->variant > 5 || cfg->split_k < 0) return QUICK_ERR_INVALID_ARG;
+    if (cfg->variant == kVariantKStream) {
+        // split_k: K slices (0 = auto; raised to the minimum); tile_n:
+        // n-tiles per wave (0 = 2); the arrival counters cover every column
+        // group
+        if (M > 16 || cfg->tile_m || (cfg->tile_n != 0 && cfg->tile_n != 1 && cfg->tile_n != 2) ||
+            cfg->split_k > KG || ks_groups(N, 1) > kSkMaxWorkgroups)
+            return QUICK_ERR_INVALID_ARG;
+        pl->variant = kVariantKStream;
+        pl->split = cfg->split_k;
+        pl->bm = 0;
+        pl->wn = cfg->tile_n ? cfg->tile_n : 2;
+        pl->kgps = 0;
+        return QUICK_OK;
+    }
     if (cfg->variant == kVariantBStream) {
         // split_k: workgroups of 8 waves (0 = one per compute unit)
         if (!bstream_lds(M, K) || cfg->split_k > kSkMaxWorkgroups / kBWaves || cfg->tile_m || cfg->tile_n)
@@ -1618,6 +1832,21 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
 void finish_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
 {
     (void)M;
+    if (pl->variant == kVariantKStream) {
+        // automatic: the fewest slices, doubled while fewer than 256
+        // workgroups exist and each slice keeps >= 4 k-groups
+        const int64_t KG = K / 128;
+        const int smin = ks_min_slices(K);
+        int s = pl->split;
+        if (!s) {
+            s = smin;
+            while ((int64_t)ks_groups(N, pl->wn) * s < 256 && KG / (2 * s) >= 4) s *= 2;
+        }
+        s = (int)std::min<int64_t>(std::max(s, smin), KG);
+        pl->kgps = ceil_div(KG, s);
+        pl->split = ceil_div(KG, pl->kgps);  // no empty slices
+        return;
+    }
     if (pl->variant == kVariantBStream) {
         if (!pl->split) pl->split = device_cus();
         // no more waves than trips of kBStreamDepth units
@@ -1653,6 +1882,8 @@ void finish_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
 size_t plan_workspace(int64_t M, int64_t N, const Plan& pl)
 {
     if (pl.variant == kVariantBStream) return kSkCounterBytes + 2 * (size_t)pl.split * kBWaves * 1024;
+    if (pl.variant == kVariantKStream && pl.split > 1)
+        return kSkCounterBytes + (size_t)ks_groups(N, pl.wn) * pl.split * kKsWaves * pl.wn * 1024;
     if (pl.variant == kVariantTiled && pl.split > 1)
         return kSkCounterBytes + (size_t)pl.split * M * N * sizeof(float);
     if (pl.variant == kVariantStreamK) return kSkCounterBytes + 2 * (size_t)pl.split * sk_slot_bytes(pl.bm, pl.wn);
@@ -1846,6 +2077,36 @@ int launch_bstream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint
     return QUICK_OK;
 }
 
+int launch_kstream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz,
+                   uint16_t* y, float* ws, int M, int N, int K, hipStream_t st, const Epi& epi)
+{
+    const int ncg = ks_groups(N, pl.wn);
+    const int64_t G = (int64_t)ncg * pl.split;
+    // partial slots addressed with 32-bit offsets
+    if (pl.split > 1 && (size_t)G * kKsWaves * pl.wn * 1024 >= ((size_t)1 << 32)) return QUICK_ERR_SHAPE;
+    // the slice: M rows x kgps k-groups of 256 bytes, whole KiB (<= 64 KiB)
+    const size_t lds = (size_t)ceil_div((int64_t)M * pl.kgps, 4) * 1024;
+    if (lds > kKsLds) return QUICK_ERR_INVALID_ARG;
+    static std::once_flag once;
+    static hipError_t attr = hipSuccess;
+    std::call_once(once, [] {
+        attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&kstream_kernel<1>),
+                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)kKsLds);
+        if (attr == hipSuccess)
+            attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&kstream_kernel<2>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kKsLds);
+    });
+    if (attr != hipSuccess) return QUICK_ERR_HIP;
+    const dim3 grid((unsigned)((G + 7) / 8 * 8));
+    if (pl.wn == 1)
+        hipLaunchKernelGGL((kstream_kernel<1>), grid, dim3(64 * kKsWaves), lds, st, x, pw, ps, pz, y, ws, M, N, K,
+                           pl.kgps, ncg, pl.split, epi);
+    else
+        hipLaunchKernelGGL((kstream_kernel<2>), grid, dim3(64 * kKsWaves), lds, st, x, pw, ps, pz, y, ws, M, N, K,
+                           pl.kgps, ncg, pl.split, epi);
+    return QUICK_OK;
+}
+
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
 
 int validate(const void* x, const void* packed, const void* scales, const void* zeros, void* y,
@@ -1884,7 +2145,7 @@ int epilogue_plan(int64_t M, int64_t N, int64_t K, const Epi& epi, const quick_c
     }
     if (!epi.act) return QUICK_OK;
     const bool fixed_n = cfg && cfg->tile_n;
-    if (pl->variant == kVariantStream && pl->wn != 2) {
+    if ((pl->variant == kVariantStream || pl->variant == kVariantKStream) && pl->wn != 2) {
         if (fixed_n) return QUICK_ERR_INVALID_ARG;
         pl->wn = 2;
     }
@@ -1934,6 +2195,8 @@ int gemm_impl(const void* x, const void* packed, const void* scales, const void*
         st = launch_stream(pl, xx, pw, ps, pz, yy, (int)M, (int)N, (int)K, hs, epi);
     else if (pl.variant == kVariantBStream)
         st = launch_bstream(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs);
+    else if (pl.variant == kVariantKStream)
+        st = launch_kstream(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs, epi);
     else
         st = launch_tiled(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs, epi);
     if (st) return st;
@@ -1985,8 +2248,8 @@ extern "C" int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config
 namespace {
 
 // Configurations worth timing for a shape: the balanced stream kernel (M <=
-// 16 with x fitting in LDS), the stream kernel (small M), the
-// tiled tiles no taller than the next power of two >= M (at least 16) with
+// 16 with x fitting in LDS), the stream kernel (small M), the sliced stream
+// kernel (M <= 16), the tiled tiles no taller than the next power of two >= M (at least 16) with
 // splits 1, 2, 4, 8 (each slice keeping >= 2 k-groups), and stream-K.
 std::vector<quick_config_t> tune_candidates(int64_t M, int64_t K)
 {
@@ -1996,6 +2259,14 @@ std::vector<quick_config_t> tune_candidates(int64_t M, int64_t K)
     if (M <= 64)
         for (int w : {1, 2, 4, 8})
             for (int p : {1, 2}) c.push_back(quick_config_t{kVariantStream, w, 0, p});
+    if (M <= 16) {
+        // sliced stream kernel: 1, 2, 4, 8 times the fewest K slices
+        const int smin = ks_min_slices(K);
+        for (int p : {1, 2})
+            for (int m = 1; m <= 8; m *= 2)
+                if ((int64_t)smin * m <= KG && (m == 1 || KG / (smin * m) >= 2))
+                    c.push_back(quick_config_t{kVariantKStream, smin * m, 0, p});
+    }
     int64_t mcap = 16;
     while (mcap < M && mcap < 128) mcap *= 2;
     static const int tiles[][2] = {{16, 16}, {16, 32}, {32, 16}, {32, 32}, {64, 32}, {64, 64}, {128, 32}};

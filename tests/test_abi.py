@@ -104,7 +104,12 @@ def test_gemm_ex_validation_without_device():
     L = Q.lib()
     def ex(cfg, M=4, N=4096, K=4096, ws=None, wsb=0):
         return L.quick_w4a16_gemm_ex(A, A, A, A, A, M, N, K, 128, None, ctypes.byref(cfg), ws, wsb)
-    assert ex(Q.make_config(variant=5)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=6)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=5), M=17) == Q.QUICK_ERR_INVALID_ARG       # more than 16 rows
+    assert ex(Q.make_config(variant=5, tile_n=3)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=5, tile_m=16)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=5, split_k=33)) == Q.QUICK_ERR_INVALID_ARG  # more slices than k-groups
+    assert ex(Q.make_config(variant=5), M=1, N=16 * 8 * 4097, K=128) == Q.QUICK_ERR_INVALID_ARG  # counters
     assert ex(Q.make_config(variant=4), M=17) == Q.QUICK_ERR_INVALID_ARG       # more than 16 rows
     assert ex(Q.make_config(variant=4), M=16, K=8192) == Q.QUICK_ERR_INVALID_ARG  # x over 128 KiB
     assert ex(Q.make_config(variant=4), K=4224) == Q.QUICK_ERR_INVALID_ARG   # K/128 not a multiple of 16
@@ -138,6 +143,16 @@ def test_gemm_ex_validation_without_device():
         Q.WS_COUNTER_BYTES + 2 * 256 * 8 * 1024
     # no more waves than trips of 16 units (2 x 16 units = 2 trips: one workgroup)
     assert Q.workspace_bytes(1, 32, 2048, Q.make_config(variant=4, split_k=64)) == Q.WS_COUNTER_BYTES + 2 * 8 * 1024
+    # sliced stream kernel: counters, then 8 waves x n-tiles per wave x 1 KiB
+    # per (column group, slice); slices raised to ceil(K/2048); one slice
+    # needs none
+    ks = Q.make_config(variant=5, split_k=8, tile_n=1)
+    assert Q.workspace_bytes(16, 528, 8192, ks) == Q.WS_COUNTER_BYTES + 5 * 8 * 8 * 1024
+    ks = Q.make_config(variant=5, split_k=1, tile_n=2)
+    assert Q.workspace_bytes(16, 528, 8192, ks) == Q.WS_COUNTER_BYTES + 3 * 4 * 8 * 2 * 1024
+    assert Q.workspace_bytes(16, 528, 2048, ks) == 0
+    # automatic slices: doubled from 2 while < 256 workgroups and >= 4 k-groups per slice
+    assert Q.workspace_bytes(1, 4096, 4096, Q.make_config(variant=5)) == Q.WS_COUNTER_BYTES + 16 * 8 * 8 * 2 * 1024
     # fewer than 8 units: one workgroup per tile, no workspace
     assert Q.workspace_bytes(16, 128, 512, Q.make_config(variant=3, tile_m=16, tile_n=16)) == 0
 

@@ -129,12 +129,13 @@ def test_c1_toy_full_output():
 
 
 @pytest.mark.parametrize("cfg", [None, dict(variant=1, split_k=4, tile_n=2), dict(variant=2, tile_m=64, tile_n=32, split_k=2),
-                                 dict(variant=2, tile_m=128, tile_n=32, split_k=1), dict(variant=4, split_k=3)])
+                                 dict(variant=2, tile_m=128, tile_n=32, split_k=1), dict(variant=4, split_k=3),
+                                 dict(variant=5, split_k=3, tile_n=1), dict(variant=5, split_k=1, tile_n=2)])
 def test_one_hot_rows_give_exact_dequant(cfg):
     """x row m = e_{k_m}: y[m][n] is a single product, so it must equal the
     binary16 rounding of (q - z) * s exactly."""
     K, N = (2048 if cfg and cfg["variant"] == 4 else 512), 96
-    M = 16 if cfg is None or cfg["variant"] in (1, 4) else 100
+    M = 16 if cfg is None or cfg["variant"] in (1, 4, 5) else 100
     g = np.random.Generator(np.random.PCG64(5))
     _, q, z, s = rand_case(6, 1, K, N)
     ks = g.choice(K, size=M, replace=False)
@@ -146,11 +147,15 @@ def test_one_hot_rows_give_exact_dequant(cfg):
     assert np.array_equal(y, want), "dequantized value mismatch at %d entries" % int((y != want).sum())
 
 
-@pytest.mark.parametrize("cfg", [None] + STREAM_CFGS[::3] + TILED_CFGS[::3] + STREAMK_CFGS[::4] + BSTREAM_CFGS)
+KSTREAM_EXACT = [dict(variant=5, split_k=1, tile_n=2), dict(variant=5, split_k=5, tile_n=1)]
+
+
+@pytest.mark.parametrize("cfg", [None] + STREAM_CFGS[::3] + TILED_CFGS[::3] + STREAMK_CFGS[::4] + BSTREAM_CFGS +
+                         KSTREAM_EXACT)
 def test_integer_data_exact_under_any_split(cfg):
     """s = 1, z = 8, q in {7,8,9}, x in {-1,0,1}: every partial sum is a small
     integer, so any summation order is exact and y equals int64 x . (q - z)."""
-    M = 48 if cfg is None or cfg["variant"] == 1 else 16 if cfg["variant"] == 4 else 150
+    M = 48 if cfg is None or cfg["variant"] == 1 else 16 if cfg["variant"] in (4, 5) else 150
     K, N = (2048 if cfg and cfg["variant"] == 4 else 1024), 80
     g = np.random.Generator(np.random.PCG64(9))
     xi = g.integers(-1, 2, (M, K))
