@@ -75,6 +75,10 @@ def launch_sequence(points):
         sel = p["sel"]
         if sel["variant"] == 1:
             seq.append((p["kernel"], "stream_kernel<"))
+        elif sel["variant"] == 4:
+            seq.append((p["kernel"], "bstream_kernel<"))
+        elif sel["variant"] == 5:
+            seq.append((p["kernel"], "kstream_kernel<%d>" % sel["tile_n"]))
         else:
             seq.append((p["kernel"], "tiled_kernel<%d, %d, 0, false, false>" % (sel["tile_m"], sel["tile_n"])))
             if sel["variant"] == 2 and sel["split_k"] > 1:
