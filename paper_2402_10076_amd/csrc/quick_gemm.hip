@@ -1647,23 +1647,43 @@ int tiled_resident(int bm, int wn)
     return g;
 }
 
+// The stream kernel's automatic shape: 2 n-tiles per wave for wide N, and
+// waves per workgroup doubled while there are fewer than 2048 waves and
+// each keeps >= 2 k-groups.
+void stream_defaults(int64_t N, int64_t K, Plan* pl)
+{
+    const int64_t KG = K / 128;
+    const int64_t NT = N / 16;
+    pl->variant = kVariantStream;
+    pl->wn = NT / 2 >= 512 ? 2 : 1;
+    const int64_t wgs = (NT + pl->wn - 1) / pl->wn;
+    int w = 1;
+    while (w < 8 && wgs * w < 2048 && KG / (2 * w) >= 2) w *= 2;
+    pl->split = w;
+    pl->bm = 0;
+    pl->kgps = 0;
+}
+
 int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
 {
     const int64_t KG = K / 128;
     const int64_t NT = N / 16;
-    auto stream_plan = [&]() {
-        pl->variant = kVariantStream;
-        pl->wn = NT / 2 >= 512 ? 2 : 1;
-        const int64_t wgs = (NT + pl->wn - 1) / pl->wn;
-        int w = 1;
-        while (w < 8 && wgs * w < 2048 && KG / (2 * w) >= 2) w *= 2;
-        pl->split = w;
-        pl->bm = 0;
-        pl->kgps = 0;
-    };
+    auto stream_plan = [&]() { stream_defaults(N, K, pl); };
     if (M <= 8) {
         // weights dominate; each wave streams its own k-range (no LDS tile)
         stream_plan();
+        return QUICK_OK;
+    }
+    if (M <= 16 && K * N / 2 < ((int64_t)128 << 20) &&
+        (int64_t)ks_groups(N, 1) * ks_min_slices(K) >= 128 && ks_groups(N, 1) <= kSkMaxWorkgroups) {
+        // sliced stream kernel, one n-tile per wave, the fewest K slices (at
+        // least 128 workgroups); the largest weight matrices stay on the
+        // 16-row tiles, which stream them as fast
+        pl->variant = kVariantKStream;
+        pl->split = 0;
+        pl->bm = 0;
+        pl->wn = 1;
+        pl->kgps = 0;
         return QUICK_OK;
     }
     // Tiled kernel: an 8-wave workgroup computes BM x (8*WN), sharing one
@@ -1784,8 +1804,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
     }
     if (cfg->variant == kVariantStream) {
         if (M > 64) return QUICK_ERR_INVALID_ARG;
-        if (pl->variant != kVariantStream) auto_plan(std::min<int64_t>(M, 64), N, K, pl);
-        pl->variant = kVariantStream;
+        if (pl->variant != kVariantStream) stream_defaults(N, K, pl);
         if (cfg->split_k) {
             if (cfg->split_k != 1 && cfg->split_k != 2 && cfg->split_k != 4 && cfg->split_k != 8)
                 return QUICK_ERR_INVALID_ARG;
@@ -1833,16 +1852,11 @@ void finish_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
 {
     (void)M;
     if (pl->variant == kVariantKStream) {
-        // automatic: the fewest slices, doubled while fewer than 256
-        // workgroups exist and each slice keeps >= 4 k-groups
+        // automatic: the fewest slices (the best or within 6 % of the best
+        // slice count on the bench shapes at M = 16)
         const int64_t KG = K / 128;
         const int smin = ks_min_slices(K);
-        int s = pl->split;
-        if (!s) {
-            s = smin;
-            while ((int64_t)ks_groups(N, pl->wn) * s < 256 && KG / (2 * s) >= 4) s *= 2;
-        }
-        s = (int)std::min<int64_t>(std::max(s, smin), KG);
+        const int s = (int)std::min<int64_t>(std::max(pl->split, smin), KG);
         pl->kgps = ceil_div(KG, s);
         pl->split = ceil_div(KG, pl->kgps);  // no empty slices
         return;

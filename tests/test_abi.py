@@ -151,8 +151,8 @@ def test_gemm_ex_validation_without_device():
     ks = Q.make_config(variant=5, split_k=1, tile_n=2)
     assert Q.workspace_bytes(16, 528, 8192, ks) == Q.WS_COUNTER_BYTES + 3 * 4 * 8 * 2 * 1024
     assert Q.workspace_bytes(16, 528, 2048, ks) == 0
-    # automatic slices: doubled from 2 while < 256 workgroups and >= 4 k-groups per slice
-    assert Q.workspace_bytes(1, 4096, 4096, Q.make_config(variant=5)) == Q.WS_COUNTER_BYTES + 16 * 8 * 8 * 2 * 1024
+    # automatic slices: the fewest (K / 2048 rounded up), two n-tiles per wave
+    assert Q.workspace_bytes(1, 4096, 4096, Q.make_config(variant=5)) == Q.WS_COUNTER_BYTES + 16 * 2 * 8 * 2 * 1024
     # fewer than 8 units: one workgroup per tile, no workspace
     assert Q.workspace_bytes(16, 128, 512, Q.make_config(variant=3, tile_m=16, tile_n=16)) == 0
 
@@ -256,6 +256,15 @@ def test_select_config_regimes():
     assert small["variant"] == Q.VARIANT_STREAM
     assert large["variant"] == Q.VARIANT_TILED
     assert Q.workspace_bytes(1, 8192, 8192) == 0
+    # 9 <= M <= 16: the sliced stream kernel (one n-tile per wave, the fewest
+    # slices) unless it would have fewer than 128 workgroups or the weights
+    # reach 128 MiB
+    assert Q.select_config(16, 12288, 4096) == dict(variant=Q.VARIANT_KSTREAM, split_k=2, tile_m=0, tile_n=1)
+    assert Q.select_config(9, 8192, 28672) == dict(variant=Q.VARIANT_KSTREAM, split_k=14, tile_m=0, tile_n=1)
+    assert Q.select_config(16, 4096, 4096)["variant"] == Q.VARIANT_STREAM      # 32 x 2 workgroups
+    assert Q.select_config(16, 57344, 8192)["variant"] == Q.VARIANT_TILED      # 224 MiB of weights
+    # an explicit stream-kernel choice with its fields left 0 takes the stream defaults
+    assert Q.workspace_bytes(16, 12288, 4096, Q.make_config(variant=1)) == 0
 
 
 def test_status_strings():

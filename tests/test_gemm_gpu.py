@@ -118,6 +118,16 @@ def test_auto_config_small_shapes(M):
     _check(M, 1024, 272, None, seed=M)
 
 
+@pytest.mark.parametrize("M", [9, 16])
+def test_auto_config_sliced_stream_shapes(M):
+    """Shapes the automatic plan gives the sliced stream kernel (>= 128
+    workgroups), and an explicit stream-kernel choice with its other fields
+    left to the defaults."""
+    assert Q.select_config(M, 8192, 4096)["variant"] == Q.VARIANT_KSTREAM
+    _check(M, 4096, 8192, None, seed=40 + M)
+    _check(M, 2048, 272, dict(variant=1), seed=50 + M)
+
+
 def test_c1_toy_full_output():
     """16 x 512 x 512, group 128, full output against the oracle."""
     import workloads as W

@@ -28,7 +28,9 @@ def test_automatic_plans_are_valid_explicit_plans(seed):
         sel = Q.select_config(M, N, K)
         cfg = Q.make_config(**sel)
         assert Q.workspace_bytes(M, N, K, cfg) == Q.workspace_bytes(M, N, K), (M, N, K, sel)
-        assert sel["variant"] in (Q.VARIANT_STREAM, Q.VARIANT_TILED, Q.VARIANT_STREAMK), sel
+        assert sel["variant"] in (Q.VARIANT_STREAM, Q.VARIANT_TILED, Q.VARIANT_STREAMK, Q.VARIANT_KSTREAM), sel
+        if sel["variant"] == Q.VARIANT_KSTREAM:
+            assert 9 <= M <= 16 and sel["split_k"] == -(-K // 2048)
 
 
 def _owner(u, W, U):
@@ -198,3 +200,63 @@ def test_bstream_ranges_pieces_and_slots(NT, KG, G):
         w1 = (((tb + KG - 1) // D + 1) * W - 1) // UD
         assert w0 <= gw <= w1 < W
         assert slot == 2 * gw + (0 if (gw * UD // W) * D >= tb else 1)
+
+
+def kstream_partition(M, N, K, npw, split):
+    """Sliced stream kernel: the host's slice count and grid, then, per
+    workgroup id, the kernel's (slice, column group), its waves' n-tiles and
+    k-groups, its slice copy and its partial slots."""
+    KG, NT = K // 128, N // 16
+    kmax = 16
+    smin = -(-KG // kmax)
+    S = min(max(split, smin), KG)
+    kgps = -(-KG // S)
+    S = -(-KG // kgps)
+    ncg = -(-NT // (8 * npw))
+    G = ncg * S
+    grid = -(-G // 8) * 8
+    lds = -(-(M * kgps) // 4) * 1024
+    assert lds <= 64 * 1024
+    wg_bytes = 8 * npw * 1024
+    covered = np.zeros((NT, KG), np.int64)
+    slots = set()
+    for b in range(grid):
+        t = (b & 7) * (grid >> 3) + (b >> 3)
+        if t >= G:
+            continue
+        s, cg = divmod(t, ncg)
+        kb = s * kgps
+        nk = min(KG, kb + kgps) - kb
+        assert 1 <= nk <= kmax
+        chunks = M * nk * 16
+        for wave in range(8):
+            i0 = wave * 64
+            while i0 < chunks:
+                for lane in range(64):
+                    idx = min(i0 + lane, chunks - 1)
+                    row, q = divmod(idx, nk * 16)
+                    qs = (q & ~15) | ((q ^ row) & 15)
+                    assert 0 <= (row * K + kb * 128 + qs * 8) * 2 < M * K * 2   # source inside x
+                    assert (i0 + lane) * 16 + 16 <= lds                         # destination inside the LDS
+                i0 += 64 * 8
+            for p in range(npw):
+                nt = cg * 8 * npw + wave * npw + p
+                if nt < NT:
+                    covered[nt, kb:kb + nk] += 1
+                if S > 1:
+                    off = (cg * S + s) * wg_bytes + (wave * npw + p) * 1024
+                    assert off + 1024 <= G * wg_bytes and off not in slots
+                    slots.add(off)
+    assert (covered == 1).all()
+    assert ncg <= 4096 and G * wg_bytes < 2 ** 32
+    return S, kgps
+
+
+@pytest.mark.parametrize("M,N,K,npw,split", [(16, 272, 4096, 1, 0), (16, 272, 4096, 2, 7), (3, 80, 2304, 1, 7),
+                                             (9, 528, 6144, 2, 1), (1, 16, 128, 1, 0), (16, 48, 28672, 2, 0),
+                                             (16, 4096, 11008, 1, 12), (16, 12288, 4096, 1, 0)])
+def test_kstream_slices_cover_every_unit_once(M, N, K, npw, split):
+    S, kgps = kstream_partition(M, N, K, npw, split)
+    cfg = Q.make_config(variant=Q.VARIANT_KSTREAM, split_k=split, tile_n=npw)
+    want = 0 if S == 1 else Q.WS_COUNTER_BYTES + -(-(N // 16) // (8 * npw)) * S * 8 * npw * 1024
+    assert Q.workspace_bytes(M, N, K, cfg) == want
