@@ -1667,7 +1667,6 @@ void stream_defaults(int64_t N, int64_t K, Plan* pl)
 int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
 {
     const int64_t KG = K / 128;
-    const int64_t NT = N / 16;
     auto stream_plan = [&]() { stream_defaults(N, K, pl); };
     if (M <= 8) {
         // weights dominate; each wave streams its own k-range (no LDS tile)
@@ -2265,7 +2264,7 @@ namespace {
 // 16 with x fitting in LDS), the stream kernel (small M), the sliced stream
 // kernel (M <= 16), the tiled tiles no taller than the next power of two >= M (at least 16) with
 // splits 1, 2, 4, 8 (each slice keeping >= 2 k-groups), and stream-K.
-std::vector<quick_config_t> tune_candidates(int64_t M, int64_t K)
+std::vector<quick_config_t> tune_candidates(int64_t M, int64_t N, int64_t K)
 {
     std::vector<quick_config_t> c;
     const int64_t KG = K / 128;
@@ -2274,12 +2273,24 @@ std::vector<quick_config_t> tune_candidates(int64_t M, int64_t K)
         for (int w : {1, 2, 4, 8})
             for (int p : {1, 2}) c.push_back(quick_config_t{kVariantStream, w, 0, p});
     if (M <= 16) {
-        // sliced stream kernel: 1, 2, 4, 8 times the fewest K slices
+        // sliced stream kernel: 1, 2, 4, 8 times the fewest K slices, and
+        // the slice counts that give about 1, 2, 3, 4 workgroups per compute
+        // unit (256 CUs)
         const int smin = ks_min_slices(K);
-        for (int p : {1, 2})
-            for (int m = 1; m <= 8; m *= 2)
-                if ((int64_t)smin * m <= KG && (m == 1 || KG / (smin * m) >= 2))
-                    c.push_back(quick_config_t{kVariantKStream, smin * m, 0, p});
+        for (int p : {1, 2}) {
+            std::vector<int> ss;
+            for (int m = 1; m <= 8; m *= 2) ss.push_back(smin * m);
+            for (int r = 1; r <= 4; ++r) ss.push_back(ceil_div(256 * r, ks_groups(N, p)));
+            std::sort(ss.begin(), ss.end());
+            int last = 0;
+            for (int s : ss) {
+                if (s < smin || s > KG || s == last || (s > smin && KG / s < 2)) continue;
+                // distinct slice lengths only
+                if (last && ceil_div(KG, ceil_div(KG, s)) == ceil_div(KG, ceil_div(KG, last))) continue;
+                c.push_back(quick_config_t{kVariantKStream, s, 0, p});
+                last = s;
+            }
+        }
     }
     int64_t mcap = 16;
     while (mcap < M && mcap < 128) mcap *= 2;
@@ -2344,7 +2355,7 @@ extern "C" int quick_tune(const void* x, const void* packed, const void* scales,
     float best_ms = 0.f;
     quick_config_t bestc{};
     bool found = false;
-    for (const quick_config_t& c : tune_candidates(M, K)) {
+    for (const quick_config_t& c : tune_candidates(M, N, K)) {
         if (st) break;
         st = gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, &c, nullptr, 0);  // warm-up
         if (st == QUICK_ERR_INVALID_ARG) {  // not supported for this shape
