@@ -160,7 +160,7 @@ def ingest_pmc(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, points, domin
     }
 
 
-def ingest_trace(trace_csv, points, dominant, out_md, command):
+def ingest_trace(trace_csv, points, dominant, out_md, command, run_log=""):
     """Kernel durations per GEMM of the step from a rocprofv3 kernel trace of
     a bench run (the run issues the step's launch sequence a whole number of
     times), written as a markdown table; returns the dominant kernel's mean
@@ -201,6 +201,14 @@ def ingest_trace(trace_csv, points, dominant, out_md, command):
             p["cid"], p["shape"], p["K"], p["N"], p["M"], p["kernel"], mu, min(per_point[i]),
             p["bytes"] / mu / 1e3, p["flops"] / mu / 1e6))
     dom_us = float(np.mean(dom_launch))
+    # the replays of the graph of the dominant kernel's launches alone, which
+    # follow the step repetitions: the launches bench.py's roofline times
+    n_dom = sum(1 for p in points if p["kernel"] == dominant)
+    dom_prefix = next(pre for b, pre in seq if b == dominant)
+    k = j
+    while k < len(rows) and dom_prefix in rows[k][1]:
+        k += 1
+    sub = [r[2] for r in rows[j:j + (k - j) // n_dom * n_dom]]
     small = [i for i, p in enumerate(points) if p["M"] <= 16]
     s_us = sum(float(np.mean(per_point[i])) for i in small)
     s_gbs = sum(points[i]["bytes"] for i in small) / s_us / 1e3
@@ -214,7 +222,20 @@ def ingest_trace(trace_csv, points, dominant, out_md, command):
                 "(tiled kernel + split-K reduction where split) over the repetitions.\n\n" % (
                     len(rows), reps, len(seq)))
         f.write("* Dominant kernel `%s`: %d launches per step, mean kernel duration **%.2f us**.\n" % (
-            dominant, sum(1 for p in points if p["kernel"] == dominant), dom_us))
+            dominant, n_dom, dom_us))
+        if sub:
+            f.write("* The same launches in the %d replays of the graph of the dominant kernel's launches alone "
+                    "(what the bench's `roofline.avg_launch_us` times): mean kernel duration **%.2f us**.\n" % (
+                        len(sub) // n_dom, float(np.mean(sub))))
+        roof = None
+        if run_log and os.path.exists(run_log):
+            for line in open(run_log, errors="replace"):
+                if line.startswith("{") and '"roofline"' in line:
+                    roof = json.loads(line)["roofline"]
+        if roof:
+            f.write("* bench.py's own JSON line from the profiled run: `roofline.avg_launch_us` = %.2f us "
+                    "(replay time of that graph / launches, so it also holds the gaps between launches), "
+                    "`frac` = %.4f.\n" % (roof["avg_launch_us"], roof["frac"]))
         f.write("* Sum of kernel time per step: %.1f us.\n" % tot)
         f.write("* GEMMs with M <= 16: %.1f us of kernels, %.0f GB/s of algorithmic bytes.\n\n" % (s_us, s_gbs))
         f.write("\n".join(lines) + "\n")
@@ -601,6 +622,7 @@ def main():
     ap.add_argument("--ingest-mfma", metavar="COUNTER_CSV",
                     help="per-GEMM matrix-core utilisation from a rocprofv3 --pmc run of MFMA_COUNTERS")
     ap.add_argument("--mfma-out", default=os.path.join(ROOT, "profiles", "mfma_util_bench_llama2_7b_70b.md"))
+    ap.add_argument("--trace-log", default="", help="with --ingest-trace: stdout of the profiled bench run")
     ap.add_argument("--ingest-trace", metavar="KERNEL_TRACE_CSV",
                     help="per-GEMM kernel durations from a rocprofv3 --kernel-trace run of this script")
     ap.add_argument("--trace-out", default=os.path.join(ROOT, "profiles", "bench_llama2_7b_70b_kernel_trace.md"))
@@ -624,7 +646,8 @@ def main():
             p["bytes"] = W.alg_bytes(p["M"], p["N"], p["K"])
             p["flops"] = W.flops(p["M"], p["N"], p["K"])
         print("dominant %s mean kernel duration %.2f us" % (
-            args.dominant, ingest_trace(args.ingest_trace, points, args.dominant, args.trace_out, args.trace_command)))
+            args.dominant, ingest_trace(args.ingest_trace, points, args.dominant, args.trace_out, args.trace_command,
+                                        args.trace_log)))
         return
 
     if args.ingest_mfma:

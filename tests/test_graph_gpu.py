@@ -1,7 +1,8 @@
 """GEMMs captured in a HIP graph replay the eager results bit for bit.
 
 Every kernel path (stream kernel, tiled data-parallel, split-K with its
-reduction kernel, stream-K with its arrival counters; the grouped GEMM's
+reduction kernel, stream-K and the sliced stream kernel with their arrival
+counters; the grouped GEMM's
 two-launch plan and a fused epilogue) is captured after an
 eager warm-up on the capture stream (so the library's per-stream workspace
 exists and the capture allocates nothing).  The graph is replayed several
@@ -22,6 +23,7 @@ CASES = [  # (M, K, N, cfg)
     (48, 1024, 528, dict(variant=2, tile_m=32, tile_n=16, split_k=2)),  # split-K + reduction
     (300, 2304, 528, dict(variant=3, tile_m=64, tile_n=32, split_k=24)),  # stream-K
     (256, 1024, 512, dict(variant=2, tile_m=128, tile_n=32, split_k=1)),  # data-parallel
+    (16, 6144, 528, dict(variant=5, split_k=3, tile_n=1)),              # sliced stream, last-arriver sum
 ]
 
 
