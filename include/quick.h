@@ -97,8 +97,8 @@ int quick_unpack_weights(const void* packed, const void* scales, const void* zer
  *   stream         hipStream_t passed as void*, NULL = default stream
  * M == 0 is a valid no-op.  The call returns after enqueueing; results are
  * visible after the stream is synchronized.  The library may use an internal
- * device workspace (split-K partial sums, stream-K partial tiles and arrival
- * counters), allocated (counters zeroed) on first need per
+ * device workspace (split-K partial sums, stream-K partial tiles, the sliced
+ * stream kernel's partial columns, and arrival counters), allocated (counters zeroed) on first need per
  * (device, stream) and kept until process exit; a call that grows it
  * synchronizes `stream` first.  Calls on one stream are ordered; calls on
  * different streams use different workspaces.
@@ -142,7 +142,8 @@ typedef struct quick_config {
 
 /* Same contract as quick_w4a16_gemm with an explicit kernel choice.
  * workspace/workspace_bytes: optional caller-owned device buffer (16-byte
- * aligned) for split-K partial sums or stream-K partial tiles; when NULL the
+ * aligned) for split-K partial sums, stream-K partial tiles or the sliced
+ * stream kernel's per-slice partial columns; when NULL the
  * internal workspace is used.  Its first QUICK_WORKSPACE_COUNTER_BYTES hold
  * arrival counters that must be zero before the buffer's first use (e.g.
  * allocate it zero-filled); every call leaves them zero.  Calls that share a
