@@ -179,31 +179,34 @@ def test_integer_data_exact_under_any_split(cfg):
     assert np.array_equal(f16_values(y), ref.astype(np.float64))
 
 
-@pytest.mark.parametrize("M", [7, 64, 200])
-def test_metamorphic_scale_rows_tiles(M):
+@pytest.mark.parametrize("M,cfg", [(7, None), (64, None), (200, None), (16, dict(variant=5, split_k=3, tile_n=1)),
+                                   (9, dict(variant=5, split_k=2, tile_n=2))],
+                         ids=["7", "64", "200", "16_sliced", "9_sliced"])
+def test_metamorphic_scale_rows_tiles(M, cfg):
     K, N = 768, 96
+    cfg = Q.make_config(**cfg) if cfg else None
     x, q, z, s = rand_case(11 + M, M, K, N)
     p = Packed(q, z, s)
     xd = to_dev_x(x)
-    y = from_dev_y(p.gemm(xd))
+    y = from_dev_y(p.gemm(xd, cfg=cfg))
     # doubling the scales doubles y exactly (outside the binary16 subnormal band)
     s2 = (f16_values(s) * 2).astype(np.float16).view(np.uint16)
-    y2 = run(x, q, z, s2)
+    y2 = run(x, q, z, s2, cfg)
     yv, y2v = f16_values(y), f16_values(y2)
     keep = np.abs(yv) >= 2.0 ** -14
     assert np.array_equal(y2v[keep], 2 * yv[keep])
     # permuting rows of x permutes rows of y
     perm = np.random.Generator(np.random.PCG64(M)).permutation(M)
-    yp = from_dev_y(p.gemm(to_dev_x(x[perm])))
+    yp = from_dev_y(p.gemm(to_dev_x(x[perm]), cfg=cfg))
     assert np.array_equal(yp, y[perm])
     # permuting whole 16-column tiles of (q, z, s) permutes columns of y
     tperm = np.random.Generator(np.random.PCG64(M + 1)).permutation(N // 16)
     cols = (tperm[:, None] * 16 + np.arange(16)[None, :]).reshape(-1)
-    yt = run(x, q[:, cols], z[:, cols], s[:, cols])
+    yt = run(x, q[:, cols], z[:, cols], s[:, cols], cfg)
     assert np.array_equal(yt, y[:, cols])
     # determinism
     for _ in range(3):
-        assert np.array_equal(from_dev_y(p.gemm(xd)), y)
+        assert np.array_equal(from_dev_y(p.gemm(xd, cfg=cfg)), y)
     torch.cuda.synchronize()
 
 
