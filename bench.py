@@ -565,6 +565,7 @@ def cpu_baseline(points, threads: int, col_fraction: float):
     import oracle
     import workloads as W
     t_total = 0.0
+    t_extra = 0.0   # each point's time scaled to all N columns
     fl_total = 0
     cache = {}
     for p in points:
@@ -580,9 +581,21 @@ def cpu_baseline(points, threads: int, col_fraction: float):
         cols = W.sample_columns(p["N"], ncols, seed=1)
         t0 = time.perf_counter()
         oracle.gemm(x[:p["M"]], q, z, s, cols=cols, threads=threads)
-        t_total += time.perf_counter() - t0
+        dt = time.perf_counter() - t0
+        t_total += dt
+        t_extra += dt * p["N"] / len(cols)
         fl_total += 2 * p["M"] * len(cols) * p["K"]
-    return fl_total, t_total
+    return fl_total, t_total, t_extra
+
+
+def cpu_c1_one_thread():
+    """The oracle on the 16 x 512 x 512 configuration, all columns, one thread."""
+    import oracle
+    import workloads as W
+    x, q, z, s = W.shape_inputs(W.C1, 0, 16)
+    t0 = time.perf_counter()
+    oracle.gemm(x, q, z, s, threads=1)
+    return time.perf_counter() - t0
 
 
 def main():
@@ -922,11 +935,13 @@ def main():
         threads = min(16, len(os.sched_getaffinity(0)))
         log("cpu baseline: oracle on %d threads, %.4f of the columns of every GEMM" % (
             threads, args.cpu_col_fraction))
-        fl, t = cpu_baseline(points, threads, args.cpu_col_fraction)
+        fl, t, t_full = cpu_baseline(points, threads, args.cpu_col_fraction)
         out["cpu_baseline"] = {
             "value": round(fl / t / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": "every GEMM of the step, all rows, a seeded sample of ceil(N/%d) columns "
                       "(%.1f GFLOP in %.1f s)" % (round(1 / args.cpu_col_fraction), fl / 1e9, t),
+            "step_s_extrapolated": round(t_full, 1),
+            "c1_16x512x512_one_thread_s": round(cpu_c1_one_thread(), 4),
         }
 
     if args.points_out:
