@@ -41,8 +41,26 @@
 #include "quick_fused.h"
 #include "quick_grouped.h"
 #include "quick_internal.h"
+#include "quick_launch.h"
+
+// The build compiles this file as three translation units in parallel
+// (QUICK_PART 0: host code and the C ABI; 1: stream-kernel launches; 2:
+// tiled-kernel launches); without QUICK_PART it is the whole library.
+#if !defined(QUICK_PART)
+#define QUICK_HOST 1
+#define QUICK_STREAM 1
+#define QUICK_TILED 1
+#else
+#define QUICK_HOST (QUICK_PART == 0)
+#define QUICK_STREAM (QUICK_PART == 1)
+#define QUICK_TILED (QUICK_PART == 2)
+#endif
 
 namespace {
+
+using quick::Epi;
+using quick::GroupArgs;
+using quick::Plan;
 
 typedef _Float16 h2_t __attribute__((ext_vector_type(2)));
 typedef _Float16 h8_t __attribute__((ext_vector_type(8)));
@@ -135,18 +153,6 @@ __device__ __forceinline__ void store_h4(uint16_t* dst, const f4_t& v)
     o[1] = (uint32_t)bits_as<uint16_t>(c) | ((uint32_t)bits_as<uint16_t>(e) << 16);
     *reinterpret_cast<u2_t*>(dst) = o;
 }
-
-// Output epilogue applied to the fp32 accumulators before the single
-// rounding to f16: an optional per-column bias, then either nothing or the
-// gated SiLU of a fused gate/up projection whose packed columns alternate
-// in 16-column tiles (gate tile t at packed columns 32t .. 32t+15, the
-// matching up tile at 32t+16 .. 32t+31):
-//   y[m][16t + i] = silu(h[m][32t + i]) * h[m][32t + 16 + i],
-//   silu(a) = a / (1 + e^-a),  h = x . W (+ bias).
-struct Epi {
-    const uint16_t* bias;  // f16 [N] in packed column order, or null
-    int act;               // 0 none, 1 gated SiLU (output has N/2 columns)
-};
 
 __device__ __forceinline__ f4_t add_bias(f4_t v, const uint16_t* bias, int n)
 {
@@ -601,26 +607,8 @@ constexpr int kSkMaxWorkgroups = 4096;
 constexpr size_t kSkCounterBytes = QUICK_WORKSPACE_COUNTER_BYTES;
 static_assert(kSkCounterBytes >= kSkMaxWorkgroups * sizeof(unsigned), "one counter per workgroup");
 constexpr int kCoherentAux = 0x11;  // sc0 sc1: coherent across XCDs, write-through
-
-// Grouped (mixture-of-experts) form: E experts' packed weights back to back,
-// routed row r of the output multiplies token rows[r] of x (row r when rows
-// is null) with the weights of the expert e whose range
-// [offsets[e], offsets[e+1]) holds r.  The per-expert row counts live only
-// in device memory: each workgroup derives the tile list from them.
 constexpr int kMaxExperts = QUICK_MAX_EXPERTS;
-struct GroupArgs {
-    const int* rows;     // [routed] token row of each routed row, or null
-    const int* offsets;  // [experts + 1] first routed row of each expert
-    int experts;
-    int routed;          // rows of y
-    // Which of each expert's rows this launch covers.  0: all.  With
-    // `unit` rows per full tile: 1 = the leading whole tiles, plus the
-    // remainder when it holds at least `keep` rows; 2 = the rest (a
-    // remainder of fewer than `keep` rows), for a launch with shorter tiles.
-    int part;
-    int unit;
-    int keep;
-};
+
 
 // WB != 0 builds the write-back ablation of the conventional design (the
 // dequantized weights go through an LDS tile and are read back as matrix
@@ -1363,7 +1351,7 @@ bstream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 // ---------------------------------------------------------------------------
 constexpr int kKsWaves = 8;
 constexpr int kKsMaxKg = kStreamSinglePass;   // k-groups per slice
-constexpr size_t kKsLds = 64 * 1024;          // LDS bytes for the slice (16 rows x 16 k-groups)
+[[maybe_unused]] constexpr size_t kKsLds = 64 * 1024;          // LDS bytes for the slice (16 rows x 16 k-groups)
 
 template <int NPW>
 __global__ void __launch_bounds__(64 * kKsWaves)
@@ -1556,7 +1544,7 @@ splitk_reduce_kernel(const float* __restrict__ ws, uint16_t* __restrict__ y, int
 // Host side: validation, configuration, workspace, launch.
 // ---------------------------------------------------------------------------
 constexpr int kVariantStream = 1;
-constexpr size_t kStreamLdsX = 64 * 1024;  // LDS bytes the stream kernel may give to activations
+[[maybe_unused]] constexpr size_t kStreamLdsX = 64 * 1024;  // LDS bytes the stream kernel may give to activations
 constexpr int kVariantTiled = 2;
 constexpr int kVariantStreamK = 3;  // tiled kernel, stream-K schedule
 constexpr int kVariantBStream = 4;  // balanced stream kernel
@@ -1586,14 +1574,6 @@ int device_cus()
     return cus;
 }
 
-struct Plan {
-    int variant;
-    int split;  // stream: waves per workgroup; tiled: k splits; stream-K: workgroups
-    int bm;     // tiled: rows per workgroup
-    int wn;     // tiled: columns per wave; stream: n-tiles per wave
-    int kgps;   // tiled: k-groups per split
-};
-
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 // Column groups (8 waves x npw n-tiles) of the sliced stream kernel, and the
@@ -1605,6 +1585,11 @@ bool is_tiled(int variant) { return variant == kVariantTiled || variant == kVari
 
 // Bytes of one stream-K partial-tile slot.
 size_t sk_slot_bytes(int bm, int wn) { return (size_t)bm * kTiledWaves * wn * sizeof(float); }
+
+}  // namespace
+
+#if QUICK_TILED
+namespace quick {
 
 template <int BM, int WN>
 int tiled_resident_per_cu()
@@ -1646,6 +1631,13 @@ int tiled_resident(int bm, int wn)
     cache[{dev, id}] = g;
     return g;
 }
+
+}  // namespace quick
+#endif
+
+namespace {
+
+using quick::tiled_resident;
 
 // The stream kernel's automatic shape: 2 n-tiles per wave for wide N, and
 // waves per workgroup doubled while there are fewer than 2048 waves and
@@ -1942,6 +1934,11 @@ int get_workspace(size_t need, hipStream_t stream, void** out)
     return QUICK_OK;
 }
 
+}  // namespace
+
+namespace quick {
+
+#if QUICK_STREAM
 template <int MT, int NPW, int WAVES>
 void launch_stream_t(const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz,
                      uint16_t* y, int M, int N, int K, hipStream_t st, const Epi& epi)
@@ -1950,15 +1947,18 @@ void launch_stream_t(const uint16_t* x, const u4_t* pw, const uint16_t* ps, cons
     dim3 grid((NT + NPW - 1) / NPW);
     // activations staged in LDS when all of x fits (one padded slice per wave)
     const size_t xbytes = (size_t)WAVES * stream_slice_bytes(M, K / 128, WAVES);
-    if (MT == 1 && xbytes <= kStreamLdsX) {
-        constexpr int D = NPW == 1 ? 8 : 4;
-        hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D, true>), grid, dim3(64 * WAVES), xbytes, st,
-                           x, pw, ps, pz, y, M, N, K, epi);
-    } else {
-        constexpr int D = MT == 1 ? (NPW == 1 ? 8 : 4) : 2;
-        hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D, false>), grid, dim3(64 * WAVES), 0, st, x, pw, ps,
-                           pz, y, M, N, K, epi);
+    // (only single-block tiles stage x: no staged instantiation for MT > 1)
+    if constexpr (MT == 1) {
+        if (xbytes <= kStreamLdsX) {
+            constexpr int D = NPW == 1 ? 8 : 4;
+            hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D, true>), grid, dim3(64 * WAVES), xbytes, st,
+                               x, pw, ps, pz, y, M, N, K, epi);
+            return;
+        }
     }
+    constexpr int D = MT == 1 ? (NPW == 1 ? 8 : 4) : 2;
+    hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D, false>), grid, dim3(64 * WAVES), 0, st, x, pw, ps,
+                       pz, y, M, N, K, epi);
 }
 
 template <int MT, int NPW>
@@ -1995,81 +1995,6 @@ int launch_stream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint1
     case 4: return launch_stream_n<4>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st, epi);
     default: return QUICK_ERR_INVALID_ARG;
     }
-}
-
-// nm: m-tiles of the tile space (grouped: the host's upper bound, the
-// kernel derives the actual count from the expert offsets)
-template <int BM, int WN, bool GRP, bool EP>
-void launch_tiled_e(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
-                    const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
-                    const GroupArgs& ga, const Epi& epi)
-{
-    const int nm = GRP ? (int)(((int64_t)ga.routed + (int64_t)ga.experts * (BM - 1)) / BM) : ceil_div(M, BM);
-    const int nn = ceil_div(N, kTiledWaves * WN);
-    if (pl.variant == kVariantStreamK) {
-        hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP, EP>), dim3(pl.split), dim3(64 * kTiledWaves), 0, st, x,
-                           pw, ps, pz, y, ws, M, N, K, 0, nm, nn, 0, ga, epi);
-        return;
-    }
-    const int nblk = nm * nn * pl.split;
-    const int grid = ceil_div(nblk, 8) * 8;
-    hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP, EP>), dim3(grid), dim3(64 * kTiledWaves), 0, st, x, pw, ps,
-                       pz, y, ws, M, N, K, pl.kgps, nm, nn, pl.split, ga, epi);
-}
-
-// A split-K launch writes raw partial sums and its reduction pass applies
-// the epilogue, so only unsplit launches need the epilogue build.
-template <int BM, int WN, bool GRP>
-void launch_tiled_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
-                    const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
-                    const GroupArgs& ga, const Epi& epi)
-{
-    const bool split = pl.variant == kVariantTiled && pl.split > 1;
-    if ((epi.bias || epi.act) && !split)
-        launch_tiled_e<BM, WN, GRP, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, ga, epi);
-    else
-        launch_tiled_e<BM, WN, GRP, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, ga, epi);
-}
-
-// Tile shapes of the grouped form.
-bool grouped_tile_supported(int bm, int wn)
-{
-    return ((bm == 16 || bm == 32) && (wn == 16 || wn == 32)) || (bm == 64 && wn == 32) || (bm == 128 && wn == 32);
-}
-
-// ga == nullptr: the plain GEMM; otherwise the grouped form (M = token rows).
-int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
-                 const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
-                 const Epi& epi, const GroupArgs* ga = nullptr)
-{
-    if (ga) {
-        if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
-        else if (pl.bm == 16 && pl.wn == 32) launch_tiled_t<16, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
-        else if (pl.bm == 32 && pl.wn == 32) launch_tiled_t<32, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
-        else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
-        else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
-        else if (pl.bm == 128 && pl.wn == 32)
-            launch_tiled_t<128, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
-        else return QUICK_ERR_INVALID_ARG;
-    } else {
-        const GroupArgs none{nullptr, nullptr, 0, 0};
-        if (pl.bm == 16 && pl.wn == 32) launch_tiled_t<16, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
-        else if (pl.bm == 32 && pl.wn == 32) launch_tiled_t<32, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
-        else if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
-        else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
-        else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
-        else if (pl.bm == 128 && pl.wn == 32)
-            launch_tiled_t<128, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
-        else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
-        else return QUICK_ERR_INVALID_ARG;
-    }
-    if (pl.variant == kVariantTiled && pl.split > 1) {
-        const int64_t rows = ga ? ga->routed : M;
-        const int64_t quads = rows * (epi.act ? N / 2 : N) / 4;
-        hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, st,
-                           ws + kSkCounterBytes / sizeof(float), y, rows, N, pl.split, epi);
-    }
-    return QUICK_OK;
 }
 
 int launch_bstream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz,
@@ -2118,6 +2043,113 @@ int launch_kstream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint
         hipLaunchKernelGGL((kstream_kernel<2>), grid, dim3(64 * kKsWaves), lds, st, x, pw, ps, pz, y, ws, M, N, K,
                            pl.kgps, ncg, pl.split, epi);
     return QUICK_OK;
+}
+#endif  // QUICK_STREAM
+
+#if QUICK_TILED
+// nm: m-tiles of the tile space (grouped: the host's upper bound, the
+// kernel derives the actual count from the expert offsets)
+template <int BM, int WN, bool GRP, bool EP>
+void launch_tiled_e(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
+                    const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
+                    const GroupArgs& ga, const Epi& epi)
+{
+    const int nm = GRP ? (int)(((int64_t)ga.routed + (int64_t)ga.experts * (BM - 1)) / BM) : ceil_div(M, BM);
+    const int nn = ceil_div(N, kTiledWaves * WN);
+    if (pl.variant == kVariantStreamK) {
+        hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP, EP>), dim3(pl.split), dim3(64 * kTiledWaves), 0, st, x,
+                           pw, ps, pz, y, ws, M, N, K, 0, nm, nn, 0, ga, epi);
+        return;
+    }
+    const int nblk = nm * nn * pl.split;
+    const int grid = ceil_div(nblk, 8) * 8;
+    hipLaunchKernelGGL((tiled_kernel<BM, WN, 0, GRP, EP>), dim3(grid), dim3(64 * kTiledWaves), 0, st, x, pw, ps,
+                       pz, y, ws, M, N, K, pl.kgps, nm, nn, pl.split, ga, epi);
+}
+
+// A split-K launch writes raw partial sums and its reduction pass applies
+// the epilogue, so only unsplit launches need the epilogue build.
+template <int BM, int WN, bool GRP>
+void launch_tiled_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
+                    const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
+                    const GroupArgs& ga, const Epi& epi)
+{
+    const bool split = pl.variant == kVariantTiled && pl.split > 1;
+    if ((epi.bias || epi.act) && !split)
+        launch_tiled_e<BM, WN, GRP, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, ga, epi);
+    else
+        launch_tiled_e<BM, WN, GRP, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, ga, epi);
+}
+
+// Tile shapes of the grouped form.
+// ga == nullptr: the plain GEMM; otherwise the grouped form (M = token rows).
+int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps,
+                 const uint32_t* pz, uint16_t* y, float* ws, int M, int N, int K, hipStream_t st,
+                 const Epi& epi, const GroupArgs* ga)
+{
+    if (ga) {
+        if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
+        else if (pl.bm == 16 && pl.wn == 32) launch_tiled_t<16, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
+        else if (pl.bm == 32 && pl.wn == 32) launch_tiled_t<32, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
+        else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
+        else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
+        else if (pl.bm == 128 && pl.wn == 32)
+            launch_tiled_t<128, 32, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, *ga, epi);
+        else return QUICK_ERR_INVALID_ARG;
+    } else {
+        const GroupArgs none{nullptr, nullptr, 0, 0};
+        if (pl.bm == 16 && pl.wn == 32) launch_tiled_t<16, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 32 && pl.wn == 32) launch_tiled_t<32, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 128 && pl.wn == 32)
+            launch_tiled_t<128, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else return QUICK_ERR_INVALID_ARG;
+    }
+    if (pl.variant == kVariantTiled && pl.split > 1) {
+        const int64_t rows = ga ? ga->routed : M;
+        const int64_t quads = rows * (epi.act ? N / 2 : N) / 4;
+        hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, st,
+                           ws + kSkCounterBytes / sizeof(float), y, rows, N, pl.split, epi);
+    }
+    return QUICK_OK;
+}
+
+int launch_ablation(const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz, uint16_t* y,
+                    int M, int N, int K, int mode, hipStream_t st)
+{
+    const int nm = ceil_div(M, 64), nn = ceil_div(N, kTiledWaves * 32);
+    const int grid = ceil_div((int64_t)nm * nn, 8) * 8;
+    const int KG = K / 128;
+    auto args = [&](auto kern) {
+        hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * kTiledWaves), 0, st, x, pw, ps, pz, y, (float*)nullptr,
+                           M, N, K, KG, nm, nn, 1, GroupArgs{nullptr, nullptr, 0, 0}, Epi{nullptr, 0});
+    };
+    if (mode == 0) args(tiled_kernel<64, 32, 0>);
+    else if (mode == 1) args(tiled_kernel<64, 32, 1>);
+    else if (mode == 2) args(tiled_kernel<64, 32, 2>);
+    else return QUICK_ERR_INVALID_ARG;
+    return QUICK_OK;
+}
+
+#endif  // QUICK_TILED
+
+}  // namespace quick
+
+#if QUICK_HOST
+namespace {
+
+using quick::launch_ablation;
+using quick::launch_bstream;
+using quick::launch_kstream;
+using quick::launch_stream;
+using quick::launch_tiled;
+
+bool grouped_tile_supported(int bm, int wn)
+{
+    return ((bm == 16 || bm == 32) && (wn == 16 || wn == 32)) || (bm == 64 && wn == 32) || (bm == 128 && wn == 32);
 }
 
 bool aligned(const void* p, uintptr_t a) { return ((uintptr_t)p % a) == 0; }
@@ -2478,20 +2510,11 @@ extern "C" int quick_ablation_gemm(const void* x, const void* packed, const void
     if (st) return st;
     if (mode < 0 || mode > 2) return QUICK_ERR_INVALID_ARG;
     if (M == 0) return QUICK_OK;
-    const int nm = ceil_div(M, 64), nn = ceil_div(N, kTiledWaves * 32);
-    const int grid = ceil_div((int64_t)nm * nn, 8) * 8;
-    const int KG = (int)(K / 128);
-    auto args = [&](auto kern) {
-        hipLaunchKernelGGL(kern, dim3(grid), dim3(64 * kTiledWaves), 0, (hipStream_t)stream,
-                           static_cast<const uint16_t*>(x), static_cast<const u4_t*>(packed),
-                           static_cast<const uint16_t*>(scales), static_cast<const uint32_t*>(zeros),
-                           static_cast<uint16_t*>(y), (float*)nullptr, (int)M, (int)N, (int)K, KG, nm, nn, 1,
-                           GroupArgs{nullptr, nullptr, 0, 0}, Epi{nullptr, 0});
-    };
     (void)hipGetLastError();
-    if (mode == 0) args(tiled_kernel<64, 32, 0>);
-    else if (mode == 1) args(tiled_kernel<64, 32, 1>);
-    else args(tiled_kernel<64, 32, 2>);
+    st = launch_ablation(static_cast<const uint16_t*>(x), static_cast<const u4_t*>(packed),
+                         static_cast<const uint16_t*>(scales), static_cast<const uint32_t*>(zeros),
+                         static_cast<uint16_t*>(y), (int)M, (int)N, (int)K, mode, (hipStream_t)stream);
+    if (st) return st;
     return hipGetLastError() == hipSuccess ? QUICK_OK : QUICK_ERR_HIP;
 }
 
@@ -2773,3 +2796,5 @@ extern "C" int quick_interleave_gate_up(const uint8_t* q_gate, const uint8_t* z_
     cols(s_gate, s_up, s, K / group);
     return QUICK_OK;
 }
+
+#endif  // QUICK_HOST
