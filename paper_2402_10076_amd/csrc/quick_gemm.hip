@@ -1784,7 +1784,9 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
     }
     if (cfg->variant == kVariantBStream) {
         // split_k: workgroups of 8 waves (0 = one per compute unit)
-        if (!bstream_lds(M, K) || cfg->split_k > kSkMaxWorkgroups / kBWaves || cfg->tile_m || cfg->tile_n)
+        // (M = 0, a no-op, is checked as one row)
+        if (!bstream_lds(std::max<int64_t>(M, 1), K) || cfg->split_k > kSkMaxWorkgroups / kBWaves || cfg->tile_m ||
+            cfg->tile_n)
             return QUICK_ERR_INVALID_ARG;
         pl->variant = kVariantBStream;
         pl->split = cfg->split_k;

@@ -275,3 +275,12 @@ def test_m_zero_is_noop():
     p = Packed(q, z, s)
     y = p.gemm(torch.empty((0, K), dtype=torch.float16, device="cuda"))
     assert tuple(y.shape) == (0, N)
+    # every explicit kernel choice (K a multiple of 2048 for the balanced stream kernel)
+    K = 2048
+    _, q, z, s = rand_case(2, 1, K, N)
+    p = Packed(q, z, s)
+    for cfg in (dict(variant=1), dict(variant=4), dict(variant=5, split_k=2), dict(variant=3, tile_m=16, tile_n=16),
+                dict(variant=2, tile_m=128, tile_n=32, split_k=2)):
+        y = p.gemm(torch.empty((0, K), dtype=torch.float16, device="cuda"), cfg=Q.make_config(**cfg))
+        assert tuple(y.shape) == (0, N)
+    torch.cuda.synchronize()
