@@ -32,6 +32,7 @@
 #include <cstring>
 #include <map>
 #include <mutex>
+#include <set>
 #include <type_traits>
 #include <utility>
 #include <vector>
@@ -1941,6 +1942,21 @@ int get_workspace(size_t need, hipStream_t stream, void** out)
 namespace quick {
 
 #if QUICK_STREAM
+// Raise a kernel's dynamic-LDS limit to `bytes`, once per (device, kernel):
+// the attribute belongs to the device that is current when it is set.
+bool lds_limit_set(const void* fn, size_t bytes)
+{
+    static std::mutex mu;
+    static std::set<std::pair<int, const void*>> done;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return false;
+    std::lock_guard<std::mutex> lk(mu);
+    if (done.count({dev, fn})) return true;
+    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)bytes) != hipSuccess) return false;
+    done.insert({dev, fn});
+    return true;
+}
+
 template <int MT, int NPW, int WAVES>
 void launch_stream_t(const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz,
                      uint16_t* y, int M, int N, int K, hipStream_t st, const Epi& epi)
@@ -2005,13 +2021,8 @@ int launch_bstream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint
     const size_t lds = bstream_lds(M, K);
     if (!lds) return QUICK_ERR_INVALID_ARG;
     // more than the default 64 KiB of dynamic LDS needs the kernel's limit raised
-    static std::once_flag once;
-    static hipError_t attr = hipSuccess;
-    std::call_once(once, [] {
-        attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&bstream_kernel<kBStreamDepth>),
-                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)kBStreamLdsX);
-    });
-    if (attr != hipSuccess) return QUICK_ERR_HIP;
+    if (!lds_limit_set(reinterpret_cast<const void*>(&bstream_kernel<kBStreamDepth>), kBStreamLdsX))
+        return QUICK_ERR_HIP;
     hipLaunchKernelGGL((bstream_kernel<kBStreamDepth>), dim3(pl.split), dim3(64 * kBWaves), lds, st, x, pw, ps, pz,
                        y, ws, M, N, K);
     return QUICK_OK;
@@ -2027,16 +2038,10 @@ int launch_kstream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint
     // the slice: M rows x kgps k-groups of 256 bytes, whole KiB (<= 64 KiB)
     const size_t lds = (size_t)ceil_div((int64_t)M * pl.kgps, 4) * 1024;
     if (lds > kKsLds) return QUICK_ERR_INVALID_ARG;
-    static std::once_flag once;
-    static hipError_t attr = hipSuccess;
-    std::call_once(once, [] {
-        attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&kstream_kernel<1>),
-                                   hipFuncAttributeMaxDynamicSharedMemorySize, (int)kKsLds);
-        if (attr == hipSuccess)
-            attr = hipFuncSetAttribute(reinterpret_cast<const void*>(&kstream_kernel<2>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)kKsLds);
-    });
-    if (attr != hipSuccess) return QUICK_ERR_HIP;
+    if (!lds_limit_set(pl.wn == 1 ? reinterpret_cast<const void*>(&kstream_kernel<1>)
+                                  : reinterpret_cast<const void*>(&kstream_kernel<2>),
+                       kKsLds))
+        return QUICK_ERR_HIP;
     const dim3 grid((unsigned)((G + 7) / 8 * 8));
     if (pl.wn == 1)
         hipLaunchKernelGGL((kstream_kernel<1>), grid, dim3(64 * kKsWaves), lds, st, x, pw, ps, pz, y, ws, M, N, K,
