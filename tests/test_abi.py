@@ -305,3 +305,27 @@ def test_tune_table_load_select_save(tmp_path):
             Q.tune_table_load(str(tmp_path / "missing.txt"))
     finally:
         Q.tune_table_clear()
+
+
+def test_committed_tune_table_entries_are_valid_plans():
+    """Every entry of the committed tune table is a configuration the
+    planner accepts for its shape: with the table loaded, the automatic
+    choice for each shape is that entry (an entry the planner rejected would
+    fall back to the built-in rules)."""
+    import os
+    path = os.path.join(os.path.dirname(Q.__file__), "tune_mi355x.txt")
+    lines = open(path).read().split("\n")
+    assert lines[0] == "quick-tune 1"
+    entries = [tuple(int(v) for v in l.split()) for l in lines[1:] if l.strip()]
+    assert len(entries) == 44
+    Q.tune_table_clear()
+    try:
+        Q.tune_table_load(path)
+        assert Q.tune_table_size() == len(entries)
+        for M, N, K, variant, split, tm, tn in entries:
+            sel = Q.select_config(M, N, K)
+            assert (sel["variant"], sel["tile_m"], sel["tile_n"]) == (variant, tm, tn), (M, N, K, sel)
+            if variant == Q.VARIANT_STREAM:
+                assert sel["split_k"] == split
+    finally:
+        Q.tune_table_clear()
