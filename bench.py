@@ -49,8 +49,6 @@ def log(*a):
 def kernel_name(sel: dict) -> str:
     if sel["variant"] == 1:
         return "stream_kernel<MT,%d,%d>" % (sel["tile_n"], sel["split_k"])
-    if sel["variant"] == 4:
-        return "bstream_kernel(G=%d)" % sel["split_k"]
     if sel["variant"] == 5:
         return "kstream_kernel<%d>(S=%d)" % (sel["tile_n"], sel["split_k"])
     name = "tiled_kernel<%d,%d>" % (sel["tile_m"], sel["tile_n"])
@@ -75,8 +73,6 @@ def launch_sequence(points):
         sel = p["sel"]
         if sel["variant"] == 1:
             seq.append((p["kernel"], "stream_kernel<"))
-        elif sel["variant"] == 4:
-            seq.append((p["kernel"], "bstream_kernel<"))
         elif sel["variant"] == 5:
             seq.append((p["kernel"], "kstream_kernel<%d>" % sel["tile_n"]))
         else:
@@ -588,6 +584,17 @@ def cpu_baseline(points, threads: int, col_fraction: float):
     return fl_total, t_total, t_extra
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo)."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_c1_one_thread():
     """The oracle on the 16 x 512 x 512 configuration, all columns, one thread."""
     import oracle
@@ -882,6 +889,11 @@ def main():
         roof = dict(bound="hbm", achieved=round(ach, 1), peak=HBM_PEAK_GBS, unit="GB/s",
                     frac=round(ach / HBM_PEAK_GBS, 4), traffic=None)
     roof["traffic"] = stored_traffic(dom)
+    # the counters cannot run inside the timed bench: the figure is the stored
+    # rocprofv3 FETCH_SIZE + WRITE_SIZE measurement of this kernel source
+    roof["traffic_source"] = ("stored rocprofv3 FETCH_SIZE+WRITE_SIZE per launch, copy-calibrated, "
+                              "profiles/traffic_bench_llama2_7b_70b.json (same kernel source hash)"
+                              if roof["traffic"] is not None else "no counter run for this kernel source")
     roof["kernel"] = dom
     roof["launches_per_step"] = len(dpts)
     roof["avg_launch_us"] = round(d_ms * 1e3 / len(dpts), 2)
@@ -932,12 +944,18 @@ def main():
     }
 
     if not args.no_cpu_baseline:
-        threads = min(16, len(os.sched_getaffinity(0)))
+        # every core this process may run on, unless the host sets a smaller
+        # CPU share for it (OMP_NUM_THREADS)
+        affinity = len(os.sched_getaffinity(0))
+        share = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+        threads = min(affinity, share) if share > 0 else affinity
         log("cpu baseline: oracle on %d threads, %.4f of the columns of every GEMM" % (
             threads, args.cpu_col_fraction))
         fl, t, t_full = cpu_baseline(points, threads, args.cpu_col_fraction)
         out["cpu_baseline"] = {
             "value": round(fl / t / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "cpu_model": cpu_model(), "affinity_cores": affinity,
+            "omp_num_threads_env": os.environ.get("OMP_NUM_THREADS", ""),
             "sample": "every GEMM of the step, all rows, a seeded sample of ceil(N/%d) columns "
                       "(%.1f GFLOP in %.1f s)" % (round(1 / args.cpu_col_fraction), fl / 1e9, t),
             "step_s_extrapolated": round(t_full, 1),

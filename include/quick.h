@@ -42,6 +42,8 @@ extern "C" {
 #define QUICK_ERR_HIP 6          /* HIP runtime error (launch, allocation)   */
 #define QUICK_ERR_WORKSPACE 7    /* caller workspace missing or too small    */
 #define QUICK_ERR_IO 8           /* tune table file unreadable / malformed   */
+#define QUICK_ERR_CAPTURE 9      /* internal workspace would have to be
+                                    allocated or grown on a capturing stream */
 
 /* Human-readable name of a status code (static storage, never NULL). */
 const char* quick_status_string(int status);
@@ -98,11 +100,21 @@ int quick_unpack_weights(const void* packed, const void* scales, const void* zer
  * M == 0 is a valid no-op.  The call returns after enqueueing; results are
  * visible after the stream is synchronized.  The library may use an internal
  * device workspace (split-K partial sums, stream-K partial tiles, the sliced
- * stream kernel's partial columns, and arrival counters), allocated (counters zeroed) on first need per
- * (device, stream) and kept until process exit; a call that grows it
- * synchronizes `stream` first.  Calls on one stream are ordered; calls on
+ * stream kernel's partial columns, and arrival counters), one per (device,
+ * stream), allocated on first need (its counters cleared on `stream`) and
+ * grown when a larger plan needs more; a grown-out buffer is retired but not
+ * freed, so graphs captured earlier keep valid pointers.  Nothing is ever
+ * freed before process exit.  Calls on one stream are ordered; calls on
  * different streams use different workspaces.
- * Errors: INVALID_ARG, SHAPE, UNSUPPORTED, ALIGNMENT, HIP. */
+ * HIP graph capture: a call on a capturing stream never allocates, clears or
+ * synchronizes; when its plan needs more internal workspace than the
+ * stream's buffer holds (e.g. the first call on that stream) it enqueues
+ * nothing and returns QUICK_ERR_CAPTURE.  Warm the stream up with the same
+ * shapes before capturing, or pass a workspace (quick_w4a16_gemm_ex).  The
+ * captured launches keep using the capture stream's buffer: replays must not
+ * overlap other work that uses it (eager calls on that stream or replays of
+ * other graphs captured on it).
+ * Errors: INVALID_ARG, SHAPE, UNSUPPORTED, ALIGNMENT, HIP, CAPTURE. */
 int quick_w4a16_gemm(const void* x, const void* packed, const void* scales,
                      const void* zeros, void* y, int64_t M, int64_t N, int64_t K,
                      int64_t group, void* stream);
@@ -113,10 +125,7 @@ typedef struct quick_config {
     int variant;   /* 0 auto, 1 = stream kernel (small M), 2 = tiled kernel,
                       3 = tiled kernel with the stream-K schedule (resident
                       workgroups share the tiles x k-groups work equally),
-                      4 = balanced stream kernel (M <= 16, M*K*2 bytes
-                      <= 128 KiB and K a multiple of 2048: every wave of the
-                      chip streams an equal share of the 16 x 128 weight
-                      units),
+                      4 = reserved (rejected with INVALID_ARG),
                       5 = sliced stream kernel (M <= 16: the 8 waves of a
                       workgroup split 128 or 256 columns, workgroups split
                       K into slices of at most 2048 channels whose rows of x
@@ -124,12 +133,11 @@ typedef struct quick_config {
     int split_k;   /* variant 2: K slices across workgroups; variant 1: waves
                       per workgroup (1, 2, 4, 8); variant 3: resident
                       workgroups, a multiple of 8 up to 4096 (clamped to the
-                      number of tile x 128-channel units); variant 4:
-                      workgroups of 8 waves, up to 512 (0 = one per compute
-                      unit); variant 5: K slices (raised to at least
+                      number of tile x 128-channel units); variant 5: K
+                      slices (raised to at least
                       ceil(K/2048), at most K/128); 0 = auto                */
     int tile_m;    /* tiled kernel rows per workgroup: 16, 32, 64 or 128
-                      (variants 4 and 5: must be 0; variant 4: tile_n too);
+                      (variant 5: must be 0);
                       supported (tile_m, tile_n) pairs: (16|32, 16|32),
                       (64, 32), (64, 64), (128, 32)                         */
     int tile_n;    /* tiled kernel columns per wave: 16, 32 or 64

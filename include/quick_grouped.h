@@ -50,7 +50,7 @@ extern "C" {
  *            K % 128 == 0); group must be 128
  * R == 0 is a valid no-op.  Asynchronous on `stream` (hipStream_t as void*,
  * NULL = default stream); the library's internal workspace is used as by
- * quick_w4a16_gemm.  When the automatic choice takes 128-row tiles (about
+ * quick_w4a16_gemm (including its graph-capture rule).  When the automatic choice takes 128-row tiles (about
  * 96 or more routed rows per expert), the GEMM runs as two launches on
  * `stream`: each expert's whole 128-row tiles, and a remainder of at least
  * 64 rows, with those tiles; then the shorter remainders with 32-row tiles,
@@ -61,7 +61,7 @@ extern "C" {
  * Errors (checked before anything is enqueued): INVALID_ARG (NULL buffer),
  * SHAPE (negative sizes, E outside 1..512, K or N not multiples, T == 0 with
  * R > 0, rows NULL with T < R, 32-bit limits as quick_w4a16_gemm per
- * expert), UNSUPPORTED (group != 128), ALIGNMENT, HIP. */
+ * expert), UNSUPPORTED (group != 128), ALIGNMENT, HIP, CAPTURE. */
 int quick_w4a16_grouped_gemm(const void* x, const int32_t* rows, const int32_t* offsets, const void* packed,
                              const void* scales, const void* zeros, void* y, int64_t T, int64_t R, int64_t E,
                              int64_t N, int64_t K, int64_t group, void* stream);

@@ -40,13 +40,17 @@ QUICK_ERR_ALIGNMENT = 5
 QUICK_ERR_HIP = 6
 QUICK_ERR_WORKSPACE = 7
 QUICK_ERR_IO = 8
+QUICK_ERR_CAPTURE = 9
 
 VARIANT_AUTO = 0
 VARIANT_STREAM = 1
 VARIANT_TILED = 2
 VARIANT_STREAMK = 3
-VARIANT_BSTREAM = 4
 VARIANT_KSTREAM = 5
+
+# torch device type of every tensor whose address goes to the library (the
+# CPU tests of the argument checks substitute "meta")
+_DEVICE_TYPE = "cuda"
 
 # leading workspace bytes that hold stream-K arrival counters (QUICK_WORKSPACE_COUNTER_BYTES)
 WS_COUNTER_BYTES = 16384
@@ -58,7 +62,8 @@ _lib = None
 class QuickError(RuntimeError):
     def __init__(self, status: int, what: str):
         self.status = status
-        super().__init__("%s: %s (status %d)" % (what, status_string(status) if _lib else "?", status))
+        name = _lib.quick_status_string(int(status)).decode() if _lib is not None else "?"
+        super().__init__("%s: %s (status %d)" % (what, name, status))
 
 
 class QuickConfig(ctypes.Structure):
@@ -228,6 +233,76 @@ def _dptr(t):
     return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
 
 
+def _nbytes(t: torch.Tensor) -> int:
+    return t.numel() * t.element_size()
+
+
+def _dev(what: str, name: str, t, ref: torch.Tensor, dtype=None, nbytes: int | None = None,
+         shape: tuple | None = None):
+    """Check that ``t`` is a contiguous tensor on ``ref``'s GPU (and of the
+    given dtype, shape and minimum byte size) before its address is passed to
+    the library: the kernels size their buffer descriptors from the shape
+    arguments, so a host tensor or a short buffer would fault instead of
+    being reported."""
+    if not isinstance(t, torch.Tensor):
+        raise QuickError(QUICK_ERR_INVALID_ARG, "%s: %s must be a torch tensor" % (what, name))
+    if t.device.type != _DEVICE_TYPE or t.device != ref.device:
+        raise QuickError(QUICK_ERR_INVALID_ARG, "%s: %s must be on %s, not %s" % (what, name, ref.device, t.device))
+    if not t.is_contiguous():
+        raise QuickError(QUICK_ERR_INVALID_ARG, "%s: %s must be contiguous" % (what, name))
+    if dtype is not None and t.dtype != dtype:
+        raise QuickError(QUICK_ERR_INVALID_ARG, "%s: %s must be %s, not %s" % (what, name, dtype, t.dtype))
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise QuickError(QUICK_ERR_INVALID_ARG, "%s: %s must have shape %s, not %s" % (
+            what, name, tuple(shape), tuple(t.shape)))
+    if nbytes is not None and _nbytes(t) < nbytes:
+        raise QuickError(QUICK_ERR_SHAPE, "%s: %s holds %d bytes, needs %d" % (what, name, _nbytes(t), nbytes))
+
+
+def _check_x(what: str, x, rows_name: str = "M"):
+    if not isinstance(x, torch.Tensor) or x.device.type != _DEVICE_TYPE:
+        raise QuickError(QUICK_ERR_INVALID_ARG, "%s: x must be a tensor on the GPU" % what)
+    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
+        raise QuickError(QUICK_ERR_INVALID_ARG,
+                         "%s: x must be a contiguous [%s][K] float16 tensor" % (what, rows_name))
+
+
+def _weight_bytes(what: str, K: int, N: int, group: int):
+    """Byte sizes (packed, scales, zeros) of one K x N weight matrix (the
+    quick_packed_sizes formulas: K*N/2, K*N/64, K*N/256)."""
+    if group != 128:
+        raise QuickError(QUICK_ERR_UNSUPPORTED, "%s: group must be 128" % what)
+    if K <= 0 or N <= 0 or K % 128 or N % 16:
+        raise QuickError(QUICK_ERR_SHAPE, "%s: need K %% 128 == 0 and N %% 16 == 0 (K=%d, N=%d)" % (what, K, N))
+    return K * N // 2, K * N // 64, K * N // 256
+
+
+def _check_weights(what: str, x, packed, scales, zeros, K: int, N: int, group: int, experts: int = 1):
+    wb, sb, zb = _weight_bytes(what, K, N, group)
+    _dev(what, "packed", packed, x, nbytes=wb * experts)
+    _dev(what, "scales", scales, x, nbytes=sb * experts)
+    _dev(what, "zeros", zeros, x, nbytes=zb * experts)
+
+
+def _out(what: str, y, x, rows: int, cols: int):
+    if y is None:
+        return torch.empty((rows, cols), dtype=torch.float16, device=x.device)
+    _dev(what, "y", y, x, dtype=torch.float16, shape=(rows, cols))
+    return y
+
+
+def _ws(what: str, workspace, x):
+    if workspace is None:
+        return 0
+    _dev(what, "workspace", workspace, x)
+    return _nbytes(workspace)
+
+
+def _stream(stream, x):
+    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    return ctypes.c_void_p(st.cuda_stream)
+
+
 def w4a16_gemm(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor,
                N: int, y: torch.Tensor | None = None, group: int = 128,
                cfg: QuickConfig | None = None, workspace: torch.Tensor | None = None,
@@ -235,24 +310,17 @@ def w4a16_gemm(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zero
     """y = x . W on the GPU.  x: [M][K] float16 (contiguous, on the device);
     packed/scales/zeros: device tensors from ``to_device``.  Runs on torch's
     current stream unless ``stream`` (a torch.cuda.Stream) is given."""
-    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
-        raise QuickError(QUICK_ERR_INVALID_ARG, "w4a16_gemm: x must be a contiguous [M][K] float16 tensor")
+    what = "w4a16_gemm"
+    _check_x(what, x)
     M, K = x.shape
-    if y is None:
-        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
-    elif y.dtype != torch.float16 or tuple(y.shape) != (M, N) or not y.is_contiguous():
-        raise QuickError(QUICK_ERR_INVALID_ARG, "w4a16_gemm: y must be a contiguous [M][N] float16 tensor")
-    wb, zb, sb = packed_sizes(K, N, group)
-    for t, nb, name in ((packed, wb, "packed"), (scales, sb, "scales"), (zeros, zb, "zeros")):
-        if not t.is_contiguous() or t.numel() * t.element_size() < nb:
-            raise QuickError(QUICK_ERR_SHAPE, "w4a16_gemm: %s buffer too small or not contiguous" % name)
-    st = stream if stream is not None else torch.cuda.current_stream(x.device)
-    hs = ctypes.c_void_p(st.cuda_stream)
+    _check_weights(what, x, packed, scales, zeros, K, N, group)
+    y = _out(what, y, x, M, N)
+    wsb = _ws(what, workspace, x)
+    hs = _stream(stream, x)
     if cfg is None and workspace is None:
         rc = lib().quick_w4a16_gemm(_dptr(x), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y),
                                     M, N, K, group, hs)
     else:
-        wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
         rc = lib().quick_w4a16_gemm_ex(_dptr(x), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y),
                                        M, N, K, group, hs,
                                        ctypes.byref(cfg) if cfg is not None else None,
@@ -265,15 +333,15 @@ def tune(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zeros: tor
          y: torch.Tensor | None = None, group: int = 128, stream=None) -> dict:
     """Time every configuration for this shape on these buffers and record the
     fastest in the library's tune table (quick_tune); returns it."""
-    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
-        raise QuickError(QUICK_ERR_INVALID_ARG, "tune: x must be a contiguous [M][K] float16 tensor")
+    what = "tune"
+    _check_x(what, x)
     M, K = x.shape
-    if y is None:
-        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
-    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    _check_weights(what, x, packed, scales, zeros, K, N, group)
+    y = _out(what, y, x, M, N)
+    hs = _stream(stream, x)
     c = QuickConfig()
     _check(lib().quick_tune(_dptr(x), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y), M, N, K, group,
-                            ctypes.c_void_p(st.cuda_stream), ctypes.byref(c)), "quick_tune")
+                            hs, ctypes.byref(c)), "quick_tune")
     return c.as_dict()
 
 
@@ -281,12 +349,14 @@ def ablation_gemm(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, z
                   N: int, mode: int, y: torch.Tensor | None = None) -> torch.Tensor:
     """quick_ablation_gemm: mode 0 direct-to-register (the method), 1 / 2
     write-back through LDS with padded / unpadded rows."""
+    what = "ablation_gemm"
+    _check_x(what, x)
     M, K = x.shape
-    if y is None:
-        y = torch.empty((M, N), dtype=torch.float16, device=x.device)
-    st = torch.cuda.current_stream(x.device)
+    _check_weights(what, x, packed, scales, zeros, K, N, 128)
+    y = _out(what, y, x, M, N)
+    hs = _stream(None, x)
     _check(lib().quick_ablation_gemm(_dptr(x), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y), M, N, K,
-                                     mode, ctypes.c_void_p(st.cuda_stream)), "quick_ablation_gemm")
+                                     mode, hs), "quick_ablation_gemm")
     return y
 
 
@@ -307,6 +377,27 @@ def grouped_workspace_bytes(R: int, E: int, N: int, K: int, cfg: QuickConfig | N
     return int(lib().quick_grouped_workspace_bytes(R, E, N, K, ctypes.byref(cfg) if cfg is not None else None))
 
 
+def _grouped_args(what, x, offsets, rows, R, packed, scales, zeros, N, group):
+    """Validated (T, K, E, R) of a grouped call."""
+    _check_x(what, x, "T")
+    T, K = x.shape
+    if not isinstance(offsets, torch.Tensor) or offsets.dim() != 1 or offsets.numel() < 2:
+        raise QuickError(QUICK_ERR_INVALID_ARG, "%s: offsets must be an int32 vector of E+1 entries" % what)
+    _dev(what, "offsets", offsets, x, dtype=torch.int32)
+    E = offsets.numel() - 1
+    if rows is not None:
+        if not isinstance(rows, torch.Tensor) or rows.dim() != 1:
+            raise QuickError(QUICK_ERR_INVALID_ARG, "%s: rows must be an int32 vector" % what)
+        _dev(what, "rows", rows, x, dtype=torch.int32)
+        if R is not None and R != rows.numel():
+            raise QuickError(QUICK_ERR_SHAPE, "%s: R disagrees with rows" % what)
+        R = rows.numel()
+    elif R is None:
+        R = T
+    _check_weights(what, x, packed, scales, zeros, K, N, group, experts=E)
+    return T, K, E, R
+
+
 def grouped_gemm(x: torch.Tensor, offsets: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor,
                  zeros: torch.Tensor, N: int, rows: torch.Tensor | None = None, R: int | None = None,
                  y: torch.Tensor | None = None, group: int = 128, cfg: QuickConfig | None = None,
@@ -317,35 +408,16 @@ def grouped_gemm(x: torch.Tensor, offsets: torch.Tensor, packed: torch.Tensor, s
     x: [T][K] float16; offsets: int32 [E+1] on the device; rows: int32 [R] on
     the device, or None (row r reads x[r]; R defaults to T); packed / scales /
     zeros: the experts' buffers back to back (``pack_experts`` + ``to_device``)."""
-    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
-        raise QuickError(QUICK_ERR_INVALID_ARG, "grouped_gemm: x must be a contiguous [T][K] float16 tensor")
-    for t, name in ((offsets, "offsets"), (rows, "rows")):
-        if t is not None and (t.dtype != torch.int32 or t.dim() != 1 or not t.is_contiguous()):
-            raise QuickError(QUICK_ERR_INVALID_ARG, "grouped_gemm: %s must be a contiguous int32 vector" % name)
-    T, K = x.shape
-    E = offsets.numel() - 1
-    if rows is not None:
-        if R is not None and R != rows.numel():
-            raise QuickError(QUICK_ERR_SHAPE, "grouped_gemm: R disagrees with rows")
-        R = rows.numel()
-    elif R is None:
-        R = T
-    if y is None:
-        y = torch.empty((R, N), dtype=torch.float16, device=x.device)
-    elif y.dtype != torch.float16 or tuple(y.shape) != (R, N) or not y.is_contiguous():
-        raise QuickError(QUICK_ERR_INVALID_ARG, "grouped_gemm: y must be a contiguous [R][N] float16 tensor")
-    wb, zb, sb = packed_sizes(K, N, group)
-    for t, nb, name in ((packed, wb, "packed"), (scales, sb, "scales"), (zeros, zb, "zeros")):
-        if not t.is_contiguous() or t.numel() * t.element_size() < nb * max(E, 0):
-            raise QuickError(QUICK_ERR_SHAPE, "grouped_gemm: %s buffer too small or not contiguous" % name)
-    st = stream if stream is not None else torch.cuda.current_stream(x.device)
-    hs = ctypes.c_void_p(st.cuda_stream)
+    what = "grouped_gemm"
+    T, K, E, R = _grouped_args(what, x, offsets, rows, R, packed, scales, zeros, N, group)
+    y = _out(what, y, x, R, N)
+    wsb = _ws(what, workspace, x)
+    hs = _stream(stream, x)
     args = (_dptr(x), _dptr(rows), _dptr(offsets), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y),
             T, R, E, N, K, group, hs)
     if cfg is None and workspace is None:
         rc = lib().quick_w4a16_grouped_gemm(*args)
     else:
-        wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
         rc = lib().quick_w4a16_grouped_gemm_ex(*args, ctypes.byref(cfg) if cfg is not None else None,
                                                _dptr(workspace), wsb)
     _check(rc, "quick_w4a16_grouped_gemm")
@@ -379,27 +451,28 @@ def fused_workspace_bytes(M, N, K, cfg=None, bias=None, activation=0) -> int:
                                                  ctypes.byref(e)))
 
 
+def _check_bias(what, bias, x, n):
+    if bias is not None:
+        _dev(what, "bias", bias, x, dtype=torch.float16, nbytes=2 * n)
+
+
 def gemm_fused(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor, N: int,
                bias: torch.Tensor | None = None, activation: int = ACT_NONE, y: torch.Tensor | None = None,
                group: int = 128, cfg: QuickConfig | None = None, workspace: torch.Tensor | None = None,
                stream=None) -> torch.Tensor:
     """quick_w4a16_gemm_fused: y = epilogue(x . W + bias); ``activation`` =
     ACT_SILU_GATE gives the [M][N/2] gated SiLU of interleaved gate/up tiles."""
-    if x.dtype != torch.float16 or x.dim() != 2 or not x.is_contiguous():
-        raise QuickError(QUICK_ERR_INVALID_ARG, "gemm_fused: x must be a contiguous [M][K] float16 tensor")
-    if bias is not None and (bias.dtype != torch.float16 or not bias.is_contiguous()):
-        raise QuickError(QUICK_ERR_INVALID_ARG, "gemm_fused: bias must be a contiguous float16 tensor")
+    what = "gemm_fused"
+    _check_x(what, x)
     M, K = x.shape
-    n_out = N // 2 if activation == ACT_SILU_GATE else N
-    if y is None:
-        y = torch.empty((M, n_out), dtype=torch.float16, device=x.device)
-    elif y.dtype != torch.float16 or tuple(y.shape) != (M, n_out) or not y.is_contiguous():
-        raise QuickError(QUICK_ERR_INVALID_ARG, "gemm_fused: y must be a contiguous [M][%d] float16 tensor" % n_out)
-    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    _check_weights(what, x, packed, scales, zeros, K, N, group)
+    _check_bias(what, bias, x, N)
+    y = _out(what, y, x, M, N // 2 if activation == ACT_SILU_GATE else N)
+    wsb = _ws(what, workspace, x)
+    hs = _stream(stream, x)
     e = _epi(bias, activation)
-    wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(lib().quick_w4a16_gemm_fused(_dptr(x), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y), M, N, K,
-                                        group, ctypes.c_void_p(st.cuda_stream), ctypes.byref(e),
+                                        group, hs, ctypes.byref(e),
                                         ctypes.byref(cfg) if cfg is not None else None, _dptr(workspace), wsb),
            "quick_w4a16_gemm_fused")
     return y
@@ -412,18 +485,16 @@ def grouped_gemm_fused(x: torch.Tensor, offsets: torch.Tensor, packed: torch.Ten
                        workspace: torch.Tensor | None = None, stream=None) -> torch.Tensor:
     """quick_w4a16_grouped_gemm_fused: the grouped GEMM with the epilogue
     (bias [E][N] per expert)."""
-    T, K = x.shape
-    E = offsets.numel() - 1
-    R = rows.numel() if rows is not None else (T if R is None else R)
-    n_out = N // 2 if activation == ACT_SILU_GATE else N
-    if y is None:
-        y = torch.empty((R, n_out), dtype=torch.float16, device=x.device)
-    st = stream if stream is not None else torch.cuda.current_stream(x.device)
+    what = "grouped_gemm_fused"
+    T, K, E, R = _grouped_args(what, x, offsets, rows, R, packed, scales, zeros, N, group)
+    _check_bias(what, bias, x, E * N)
+    y = _out(what, y, x, R, N // 2 if activation == ACT_SILU_GATE else N)
+    wsb = _ws(what, workspace, x)
+    hs = _stream(stream, x)
     e = _epi(bias, activation)
-    wsb = workspace.numel() * workspace.element_size() if workspace is not None else 0
     _check(lib().quick_w4a16_grouped_gemm_fused(_dptr(x), _dptr(rows), _dptr(offsets), _dptr(packed),
                                                 _dptr(scales), _dptr(zeros), _dptr(y), T, R, E, N, K, group,
-                                                ctypes.c_void_p(st.cuda_stream), ctypes.byref(e),
+                                                hs, ctypes.byref(e),
                                                 ctypes.byref(cfg) if cfg is not None else None,
                                                 _dptr(workspace), wsb),
            "quick_w4a16_grouped_gemm_fused")

@@ -239,11 +239,14 @@ __device__ __forceinline__ void with_count(int n, F&& f)
     }
 }
 // Workgroup execution barrier without memory-fence semantics.  Used where
-// explicit counter waits already order the memory traffic: every LDS-DMA a
-// wave issued for the next stage has completed (its vmcnt wait) and every LDS
-// read of the stage about to be overwritten has returned (its data fed the
-// matrix instructions before the barrier).
+// explicit counter waits before it already order the memory traffic: every
+// LDS-DMA a wave issued for the next stage has completed (vmcnt wait) and
+// every LDS read of a stage that another wave may overwrite after the
+// barrier has returned its data (lgkmcnt wait, wait_lds()).
 __device__ __forceinline__ void barrier() { __builtin_amdgcn_s_barrier(); }
+// Wait until every LDS read of this wave has returned (lgkmcnt 0; vmcnt and
+// expcnt left at their maxima).
+__device__ __forceinline__ void wait_lds() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 // Scheduling fence: no instruction moves across it.
 __device__ __forceinline__ void sched_fence() { __builtin_amdgcn_sched_barrier(0); }
 __device__ __forceinline__ uint32_t uniform(uint32_t v) { return __builtin_amdgcn_readfirstlane(v); }
@@ -878,9 +881,13 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
                 __builtin_amdgcn_sched_group_barrier(0x002, VPER, 0); // VALU
             }
             if (j == 2) {
-                // k-group st+1 has landed for every wave, and no wave reads
-                // stage st-1 any more (its last reads came before this point)
+                // After the barrier k-group st+1 has landed for every wave,
+                // and every wave's reads of stage st (step 3, just issued)
+                // have returned, so stage st may be refilled once the next
+                // k-group starts.  The step-3 instructions below need those
+                // fragments first anyway.
                 wait_groups(wgroups);
+                wait_lds();
                 barrier();
                 sched_fence();
             }
@@ -1093,232 +1100,6 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         }
         u += ke - kb;
         __syncthreads();  // LDS stages and sk_last are reused by the next piece
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Balanced stream kernel (small M, bandwidth-bound).
-//
-// The same per-unit work as the stream kernel -- one 16-byte load per lane
-// and 1 KiB unit straight into VGPRs, dequantized there and fed to the
-// 16x16x32 instruction with the activations as the other operand -- but the
-// work is spread evenly over every wave of the chip instead of by n-tiles:
-// gridDim.x workgroups of 8 waves (one per CU), and global wave w of W owns
-// a contiguous range of the U = N/16 * K/128 units in n-major order, cut at
-// multiples of the ring depth D (W = at most U / D waves; ranges differ by
-// at most D units).  In that order the unit index is also the unit's
-// position in the packed buffers, so a wave streams one contiguous stretch
-// of memory through its register ring, across n-tile boundaries, and every
-// SIMD ends up with the same amount of work (with one workgroup per n-tile
-// pair, a count of workgroups that is not a multiple of the SIMDs leaves
-// some SIMDs with twice the work of others, and the GEMM ends when they do).
-// K/128 must be a multiple of D: n-tile boundaries then fall between trips
-// of D units, so the unrolled trip body has no branch (a branch inside it
-// makes the compiler drain the ring every trip).
-//
-// All rows of x (M <= 16, M*K*2 bytes) are copied once into LDS with the
-// 16-byte LDS-DMA load, row-major as in memory; fragments are LDS reads.
-//
-// An n-tile whose K range spans several waves: each wave writes its fp32
-// partial (16 x 16 values, one 16-byte store per lane) with device-coherent
-// stores while it keeps streaming; after its range it waits for its stores,
-// bumps the tile's arrival counter, and the last contributor to arrive adds
-// the partials in k order (deterministic), rounds once and stores y.
-// ---------------------------------------------------------------------------
-constexpr int kBWaves = 8;
-
-// s_waitcnt until at most PER * min(n, N) vector-memory operations are
-// outstanding (n <= 0: none), for a runtime n: the counter field of the
-// instruction is an immediate, so each value is its own branch.  gfx9
-// encoding: vmcnt in bits 3:0 and 15:14, expcnt and lgkmcnt at their maxima.
-template <int PER, int N>
-__device__ __forceinline__ void wait_vm_upto(int n)
-{
-    if constexpr (N == 0) {
-        wait_all();
-    } else {
-        constexpr int v = PER * N;
-        static_assert(v <= 63, "vmcnt range");
-        if (n >= N) __builtin_amdgcn_s_waitcnt(0x0F70 | (v & 15) | ((v >> 4) << 14));
-        else wait_vm_upto<PER, N - 1>(n);
-    }
-}
-
-template <int D>
-__global__ void __launch_bounds__(64 * kBWaves)
-bstream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
-               const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
-               uint16_t* __restrict__ y, float* __restrict__ ws, int M, int N, int K)
-{
-    static_assert(D % 2 == 0 && 3 * D <= 63, "ring depth: even, and its loads within the vmcnt range");
-    extern __shared__ __attribute__((aligned(1024))) uint8_t xs[];
-    const int KG = K >> 7;
-    const int NT = N >> 4;
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int c = lane & 15;
-    const int g = lane >> 4;
-    const int U = NT * KG;
-    const int UD = U / D;                               // trips of D units (KG % D == 0)
-    const int W = min((int)gridDim.x * kBWaves, UD);   // waves with work
-    const int gw = blockIdx.x * kBWaves + wave;
-    const bool active = gw < W;
-    const int u0 = active ? (int)((int64_t)gw * UD / W) * D : 0;
-    const int u1 = active ? (int)((int64_t)(gw + 1) * UD / W) * D : 0;
-
-    const rsrc_t rw = make_rsrc(pw, (uint32_t)((size_t)K * N / 2));
-    const rsrc_t rs = make_rsrc(ps, (uint32_t)((size_t)K * N / 64));
-    const rsrc_t rz = make_rsrc(pz, (uint32_t)((size_t)K * N / 256));
-    const uint32_t xbytes = (uint32_t)M * K * 2;
-    const rsrc_t rx = make_rsrc(x, xbytes);
-
-    // trips completed per wave, read by the wave sharing its SIMD (below)
-    __shared__ int trips_done[kBWaves];
-    if (lane == 0) trips_done[wave] = 0;
-    // copy x into LDS: instruction i moves bytes [1024 i, 1024 i + 1024); the
-    // allocation is rounded up to whole KiB, and the last instruction's lanes
-    // past the end re-read the final 16 bytes into that padding
-    const int nins = (int)((xbytes + 1023) / 1024);
-    for (int i = wave; i < nins; i += kBWaves)
-        dma16(rx, xs + (size_t)i * 1024, min((uint32_t)i * 1024u + lane * 16u, xbytes - 16u), 0);
-
-    // scales are loaded as the 32-bit pair holding this column's (a 16-bit
-    // load's zero extension, carried around the loop, makes the compiler
-    // wait for the whole ring every trip)
-    WStage<1> ring[D];
-    const uint32_t ssel = (c & 1) ? 0x03020302u : 0x01000100u;
-    auto load_w = [&](WStage<1>& st, int u) __attribute__((always_inline)) {
-        const uint32_t uu = uniform((uint32_t)u);
-        st.w[0] = ld128(rw, lane * 16u, uu * 1024u);
-        st.s[0] = ld32(rs, (c & ~1) * 2u, uu * 32u);
-        st.z[0] = ld32(rz, (c >> 3) * 4u, uu * 8u);
-    };
-    // prologue: the first D units of the range in flight behind the copy
-#pragma unroll
-    for (int i = 0; i < D; ++i)
-        if (u0 + i < u1) load_w(ring[i], u0 + i);
-    // this wave's copy instructions, issued before the prologue loads, have
-    // completed once at most 3 * (prologue units) loads are outstanding
-    wait_vm_upto<3, D>(u1 - u0);
-    __syncthreads();  // every wave's part of x is in LDS
-    if (!active) return;
-
-    const uint32_t xrow = (uint32_t)min(c, M - 1) * (uint32_t)K * 2u + g * 16u;
-    u4_t xf[2][4];
-    auto load_x = [&](u4_t (&xb)[4], int kg) __attribute__((always_inline)) {
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            xb[j] = *reinterpret_cast<const u4_t*>(xs + xrow + (uint32_t)kg * 256u + j * 64);
-    };
-    f4_t acc = f4_t{0.f, 0.f, 0.f, 0.f};
-    auto compute = [&](const WStage<1>& st, const u4_t (&xb)[4]) __attribute__((always_inline)) {
-        const Deq d = make_deq_pair(st.s[0], ssel, (st.z[0] >> (4 * (c & 7))) & 15u);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc = mfma16(dequant8(st.w[0][j], d), bits_as<h8_t>(xb[j]), acc);
-    };
-
-    unsigned* counters = reinterpret_cast<unsigned*>(ws);
-    const rsrc_t rp = make_rsrc(ws + kSkCounterBytes / sizeof(float), (uint32_t)(2 * W) * 1024u);
-    int nt = u0 / KG;
-    int kg = u0 - nt * KG;
-    int pstart = u0;          // first unit of the current piece
-    int part_first = -1;      // n-tile of a partial first piece, if any
-    int part_last = -1;       // n-tile of a partial last piece, if any
-    // end of a piece at unit u (the tile's last unit, or the range's)
-    auto flush = [&](int u) __attribute__((always_inline)) {
-        if (pstart == nt * KG && u == nt * KG + KG - 1) {
-            if (c < M) store_h4(y + (size_t)c * N + nt * 16 + 4 * g, acc);
-        } else {
-            const bool first = pstart == u0;
-            __builtin_amdgcn_raw_buffer_store_b128(bits_as<u4_t>(acc), rp, lane * 16u,
-                                                   uniform((uint32_t)(2 * gw + (first ? 0 : 1)) * 1024u),
-                                                   kCoherentAux);
-            if (first) part_first = nt;
-            else part_last = nt;
-        }
-        acc = f4_t{0.f, 0.f, 0.f, 0.f};
-        pstart = u + 1;
-    };
-    auto advance = [&]() __attribute__((always_inline)) {
-        if (++kg == KG) {
-            kg = 0;
-            ++nt;
-        }
-    };
-
-    load_x(xf[0], kg);
-    int u = u0;
-    // Waves w and w + 4 share a SIMD, whose issue arbiter favours the older
-    // one: left alone, the younger wave falls far behind and finishes its
-    // range alone, with half the loads in flight.  After each trip a wave
-    // publishes its progress and raises its priority while it trails its
-    // sibling, which keeps the two within about a trip of each other.
-    int trips = 0;
-    const int sib = wave ^ 4;
-    // steady state: every refill inside the range, straight-line requests;
-    // a trip starts at a multiple of D inside an n-tile, so it never crosses
-    // the n-tile's end, which can only be its last unit
-    for (; u + 2 * D <= u1; u += D) {
-#pragma unroll
-        for (int i = 0; i < D; ++i) {
-            const int kn = kg + i + 1 == KG ? 0 : kg + i + 1;
-            load_x(xf[(i + 1) & 1], kn);
-            compute(ring[i], xf[i & 1]);
-            load_w(ring[i], u + i + D);
-            sched_fence();
-        }
-        kg += D - 1;
-        if (kg == KG - 1) flush(u + D - 1);
-        advance();
-        ++trips;
-        // relaxed atomics: the sibling's count changes behind the compiler's
-        // back, and no ordering with other memory operations is needed
-        __hip_atomic_store(&trips_done[wave], trips, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
-        if (__hip_atomic_load(&trips_done[sib], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP) > trips)
-            __builtin_amdgcn_s_setprio(2);
-        else
-            __builtin_amdgcn_s_setprio(0);
-    }
-    __builtin_amdgcn_s_setprio(0);
-    // tail
-    for (; u < u1; u += D) {
-#pragma unroll
-        for (int i = 0; i < D; ++i) {
-            if (u + i < u1) {
-                const int kn = kg + 1 == KG ? 0 : kg + 1;
-                if (u + i + 1 < u1) load_x(xf[(i + 1) & 1], kn);
-                compute(ring[i], xf[i & 1]);
-                if (u + i + D < u1) load_w(ring[i], u + i + D);
-                if (kg == KG - 1 || u + i == u1 - 1) flush(u + i);
-                advance();
-            }
-        }
-    }
-
-    // fix-up of the (at most two) tiles this wave shares with other waves
-    if (part_first < 0 && part_last < 0) return;
-    wait_all();  // this wave's partials are written through
-    for (int which = 0; which < 2; ++which) {
-        const int t = which == 0 ? part_first : part_last;
-        if (t < 0) continue;
-        const int tb = t * KG;
-        // owners of the tile's first and last trips (wave w owns trips
-        // [w*UD/W, (w+1)*UD/W))
-        const int w0 = (int)(((int64_t)(tb / D + 1) * W - 1) / UD);
-        const int w1 = (int)(((int64_t)((tb + KG - 1) / D + 1) * W - 1) / UD);
-        unsigned old = 0;
-        if (lane == 0) old = __hip_atomic_fetch_add(&counters[w1], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (uniform(old) != (unsigned)(w1 - w0)) continue;
-        f4_t sum = f4_t{0.f, 0.f, 0.f, 0.f};
-        for (int w = w0; w <= w1; ++w) {
-            // w's piece of this tile is its first piece when w's range starts inside the tile
-            const int slot = 2 * w + ((int)((int64_t)w * UD / W) * D >= tb ? 0 : 1);
-            const f4_t v = bits_as<f4_t>(
-                __builtin_amdgcn_raw_buffer_load_b128(rp, lane * 16u, uniform((uint32_t)slot * 1024u), kCoherentAux));
-            sum = w == w0 ? v : sum + v;
-        }
-        if (c < M) store_h4(y + (size_t)c * N + t * 16 + 4 * g, sum);
-        if (lane == 0) __hip_atomic_store(&counters[w1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
 }
 
@@ -1548,32 +1329,9 @@ constexpr int kVariantStream = 1;
 [[maybe_unused]] constexpr size_t kStreamLdsX = 64 * 1024;  // LDS bytes the stream kernel may give to activations
 constexpr int kVariantTiled = 2;
 constexpr int kVariantStreamK = 3;  // tiled kernel, stream-K schedule
-constexpr int kVariantBStream = 4;  // balanced stream kernel
+// (variant 4, a balanced stream kernel, was withdrawn: it never won on a
+// measured shape; the number stays reserved and is rejected)
 constexpr int kVariantKStream = 5;  // sliced stream kernel
-constexpr size_t kBStreamLdsX = 128 * 1024;  // LDS bytes the balanced stream kernel may give to x
-constexpr int kBStreamDepth = 16;            // its register ring depth (units in flight per wave)
-
-// LDS bytes the balanced stream kernel stages x in (whole KiB), 0 when it
-// cannot run the shape (more than 16 rows, x too large, or K/128 not a
-// multiple of its ring depth).
-size_t bstream_lds(int64_t M, int64_t K)
-{
-    if (M < 1 || M > 16 || (K / 128) % kBStreamDepth != 0) return 0;
-    const size_t b = ((size_t)M * K * 2 + 1023) / 1024 * 1024;
-    return b <= kBStreamLdsX ? b : 0;
-}
-
-// Compute units of the current device (256 when none can be queried).
-int device_cus()
-{
-    int dev = 0, cus = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) {
-        (void)hipGetLastError();
-        return 256;
-    }
-    return cus;
-}
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
@@ -1768,7 +1526,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
     if (!cfg && tuned_config(M, N, K, &tuned)) cfg = &tuned;
     if (!cfg) return QUICK_OK;
     const int64_t KG = K / 128;
-    if (cfg->variant < 0 || cfg->variant > 5 || cfg->split_k < 0) return QUICK_ERR_INVALID_ARG;
+    if (cfg->variant < 0 || cfg->variant > 5 || cfg->variant == 4 || cfg->split_k < 0) return QUICK_ERR_INVALID_ARG;
     if (cfg->variant == kVariantKStream) {
         // split_k: K slices (0 = auto; raised to the minimum); tile_n:
         // n-tiles per wave (0 = 2); the arrival counters cover every column
@@ -1780,19 +1538,6 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
         pl->split = cfg->split_k;
         pl->bm = 0;
         pl->wn = cfg->tile_n ? cfg->tile_n : 2;
-        pl->kgps = 0;
-        return QUICK_OK;
-    }
-    if (cfg->variant == kVariantBStream) {
-        // split_k: workgroups of 8 waves (0 = one per compute unit)
-        // (M = 0, a no-op, is checked as one row)
-        if (!bstream_lds(std::max<int64_t>(M, 1), K) || cfg->split_k > kSkMaxWorkgroups / kBWaves || cfg->tile_m ||
-            cfg->tile_n)
-            return QUICK_ERR_INVALID_ARG;
-        pl->variant = kVariantBStream;
-        pl->split = cfg->split_k;
-        pl->bm = 0;
-        pl->wn = 0;
         pl->kgps = 0;
         return QUICK_OK;
     }
@@ -1855,13 +1600,6 @@ void finish_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
         pl->split = ceil_div(KG, pl->kgps);  // no empty slices
         return;
     }
-    if (pl->variant == kVariantBStream) {
-        if (!pl->split) pl->split = device_cus();
-        // no more waves than trips of kBStreamDepth units
-        const int64_t trips = (N / 16) * (K / 128) / kBStreamDepth;
-        pl->split = (int)std::max<int64_t>(1, std::min<int64_t>(pl->split, (trips + kBWaves - 1) / kBWaves));
-        return;
-    }
     if (pl->variant == kVariantStreamK) {
         // 8 <= workgroups <= tiles x k-groups, a multiple of 8: every
         // workgroup gets a non-empty range and the XCD mapping is exact
@@ -1889,7 +1627,6 @@ void finish_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
 // between calls), then split-K partial outputs or stream-K partial tiles.
 size_t plan_workspace(int64_t M, int64_t N, const Plan& pl)
 {
-    if (pl.variant == kVariantBStream) return kSkCounterBytes + 2 * (size_t)pl.split * kBWaves * 1024;
     if (pl.variant == kVariantKStream && pl.split > 1)
         return kSkCounterBytes + (size_t)ks_groups(N, pl.wn) * pl.split * kKsWaves * pl.wn * 1024;
     if (pl.variant == kVariantTiled && pl.split > 1)
@@ -1898,7 +1635,9 @@ size_t plan_workspace(int64_t M, int64_t N, const Plan& pl)
     return 0;
 }
 
-// Library-owned split-K workspace, one per (device, stream).
+// Library-owned workspace, one per (device, stream).  A buffer that a larger
+// plan outgrows is retired but never freed: a graph captured while it was
+// current keeps launching with its address.
 struct WsKey {
     int dev;
     void* stream;
@@ -1910,6 +1649,7 @@ struct WsBuf {
 };
 std::mutex g_ws_mu;
 std::map<WsKey, WsBuf> g_ws;
+std::vector<void*> g_ws_retired;
 
 int get_workspace(size_t need, hipStream_t stream, void** out)
 {
@@ -1918,19 +1658,29 @@ int get_workspace(size_t need, hipStream_t stream, void** out)
     std::lock_guard<std::mutex> lk(g_ws_mu);
     WsBuf& b = g_ws[WsKey{dev, (void*)stream}];
     if (b.bytes < need) {
-        if (b.ptr) {
-            if (hipStreamSynchronize(stream) != hipSuccess) return QUICK_ERR_HIP;
-            (void)hipFree(b.ptr);
-            b.ptr = nullptr;
-            b.bytes = 0;
-        }
-        size_t sz = std::max<size_t>(need, (size_t)1 << 20);
-        if (hipMalloc(&b.ptr, sz) != hipSuccess) {
-            b.ptr = nullptr;
+        // Allocating and clearing are not allowed on a capturing stream:
+        // the caller gets a status and nothing is enqueued.
+        hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+        if (hipStreamIsCapturing(stream, &cs) != hipSuccess) {
+            (void)hipGetLastError();
             return QUICK_ERR_HIP;
         }
-        // stream-K arrival counters start at zero (every call leaves them zero)
-        if (hipMemsetAsync(b.ptr, 0, kSkCounterBytes, stream) != hipSuccess) return QUICK_ERR_HIP;
+        if (cs != hipStreamCaptureStatusNone) return QUICK_ERR_CAPTURE;
+        const size_t sz = std::max<size_t>(need, (size_t)1 << 20);
+        void* p = nullptr;
+        if (hipMalloc(&p, sz) != hipSuccess) {
+            (void)hipGetLastError();
+            return QUICK_ERR_HIP;
+        }
+        // arrival counters start at zero (every call leaves them zero)
+        if (hipMemsetAsync(p, 0, kSkCounterBytes, stream) != hipSuccess) {
+            (void)hipGetLastError();
+            (void)hipFree(p);
+            return QUICK_ERR_HIP;
+        }
+        // work already enqueued (or captured) with the old buffer keeps it
+        if (b.ptr) g_ws_retired.push_back(b.ptr);
+        b.ptr = p;
         b.bytes = sz;
     }
     *out = b.ptr;
@@ -2013,19 +1763,6 @@ int launch_stream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint1
     case 4: return launch_stream_n<4>(pl.wn, pl.split, x, pw, ps, pz, y, M, N, K, st, epi);
     default: return QUICK_ERR_INVALID_ARG;
     }
-}
-
-int launch_bstream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz,
-                   uint16_t* y, float* ws, int M, int N, int K, hipStream_t st)
-{
-    const size_t lds = bstream_lds(M, K);
-    if (!lds) return QUICK_ERR_INVALID_ARG;
-    // more than the default 64 KiB of dynamic LDS needs the kernel's limit raised
-    if (!lds_limit_set(reinterpret_cast<const void*>(&bstream_kernel<kBStreamDepth>), kBStreamLdsX))
-        return QUICK_ERR_HIP;
-    hipLaunchKernelGGL((bstream_kernel<kBStreamDepth>), dim3(pl.split), dim3(64 * kBWaves), lds, st, x, pw, ps, pz,
-                       y, ws, M, N, K);
-    return QUICK_OK;
 }
 
 int launch_kstream(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz,
@@ -2149,7 +1886,6 @@ int launch_ablation(const uint16_t* x, const u4_t* pw, const uint16_t* ps, const
 namespace {
 
 using quick::launch_ablation;
-using quick::launch_bstream;
 using quick::launch_kstream;
 using quick::launch_stream;
 using quick::launch_tiled;
@@ -2185,16 +1921,10 @@ int validate(const void* x, const void* packed, const void* scales, const void* 
 // The epilogue's constraints on a plan.  The gated form needs each gate
 // tile and its up tile in one wave (stream kernel: 2 n-tiles per wave;
 // tiled kernel: an even number of 16-column tiles per wave) unless a split-K
-// reduction pass applies it; the balanced stream kernel has no epilogue.
-// Choices left automatic are adjusted; an explicit one that conflicts (a
-// tile_n the caller set, the balanced stream kernel) is an error.
-int epilogue_plan(int64_t M, int64_t N, int64_t K, const Epi& epi, const quick_config_t* cfg, Plan* pl)
+// reduction pass applies it.  Choices left automatic are adjusted; an
+// explicit one that conflicts (a tile_n the caller set) is an error.
+int epilogue_plan(const Epi& epi, const quick_config_t* cfg, Plan* pl)
 {
-    if (!epi.bias && !epi.act) return QUICK_OK;
-    if (pl->variant == kVariantBStream) {
-        if (cfg && cfg->variant == kVariantBStream) return QUICK_ERR_INVALID_ARG;
-        auto_plan(M, N, K, pl);
-    }
     if (!epi.act) return QUICK_OK;
     const bool fixed_n = cfg && cfg->tile_n;
     if ((pl->variant == kVariantStream || pl->variant == kVariantKStream) && pl->wn != 2) {
@@ -2220,7 +1950,7 @@ int gemm_impl(const void* x, const void* packed, const void* scales, const void*
     Plan pl;
     st = make_plan(M, N, K, cfg, &pl);
     if (st) return st;
-    st = epilogue_plan(M, N, K, epi, cfg, &pl);
+    st = epilogue_plan(epi, cfg, &pl);
     if (st) return st;
     if (M == 0) return QUICK_OK;
     finish_plan(M, N, K, &pl);
@@ -2245,8 +1975,6 @@ int gemm_impl(const void* x, const void* packed, const void* scales, const void*
     (void)hipGetLastError();  // clear a stale error so the check below is ours
     if (pl.variant == kVariantStream)
         st = launch_stream(pl, xx, pw, ps, pz, yy, (int)M, (int)N, (int)K, hs, epi);
-    else if (pl.variant == kVariantBStream)
-        st = launch_bstream(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs);
     else if (pl.variant == kVariantKStream)
         st = launch_kstream(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs, epi);
     else
@@ -2293,7 +2021,7 @@ extern "C" int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config
     cfg->variant = pl.variant;
     cfg->split_k = pl.split;
     cfg->tile_m = is_tiled(pl.variant) ? pl.bm : 0;
-    cfg->tile_n = pl.variant == kVariantBStream ? 0 : pl.wn;
+    cfg->tile_n = pl.wn;
     return QUICK_OK;
 }
 
@@ -2307,7 +2035,6 @@ std::vector<quick_config_t> tune_candidates(int64_t M, int64_t N, int64_t K)
 {
     std::vector<quick_config_t> c;
     const int64_t KG = K / 128;
-    if (bstream_lds(M, K)) c.push_back(quick_config_t{kVariantBStream, 0, 0, 0});
     if (M <= 64)
         for (int w : {1, 2, 4, 8})
             for (int p : {1, 2}) c.push_back(quick_config_t{kVariantStream, w, 0, p});
@@ -2766,7 +2493,7 @@ extern "C" size_t quick_fused_workspace_bytes(int64_t M, int64_t N, int64_t K, c
     if (M <= 0 || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return 0;
     Plan pl;
     if (make_plan(M, N, K, cfg, &pl)) return 0;
-    if (epilogue_plan(M, N, K, to_epi(epi), cfg, &pl)) return 0;
+    if (epilogue_plan(to_epi(epi), cfg, &pl)) return 0;
     finish_plan(M, N, K, &pl);
     return plan_workspace(M, N, pl);
 }

@@ -55,8 +55,6 @@ struct Plan {
 // Stream-kernel part.
 int launch_stream(const Plan& pl, const uint16_t* x, const lu4_t* pw, const uint16_t* ps, const uint32_t* pz,
                   uint16_t* y, int M, int N, int K, hipStream_t st, const Epi& epi);
-int launch_bstream(const Plan& pl, const uint16_t* x, const lu4_t* pw, const uint16_t* ps, const uint32_t* pz,
-                   uint16_t* y, float* ws, int M, int N, int K, hipStream_t st);
 int launch_kstream(const Plan& pl, const uint16_t* x, const lu4_t* pw, const uint16_t* ps, const uint32_t* pz,
                    uint16_t* y, float* ws, int M, int N, int K, hipStream_t st, const Epi& epi);
 

@@ -171,6 +171,9 @@ extern "C" const char* quick_status_string(int status)
     case QUICK_ERR_HIP: return "QUICK_ERR_HIP: HIP runtime error";
     case QUICK_ERR_WORKSPACE: return "QUICK_ERR_WORKSPACE: workspace missing or too small";
     case QUICK_ERR_IO: return "QUICK_ERR_IO: tune table file unreadable or malformed";
+    case QUICK_ERR_CAPTURE:
+        return "QUICK_ERR_CAPTURE: the internal workspace would have to be allocated or grown while the stream "
+               "is being captured (call once on that stream before capturing, or pass a workspace)";
     default: return "unknown quick status";
     }
 }

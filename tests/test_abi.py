@@ -110,11 +110,8 @@ def test_gemm_ex_validation_without_device():
     assert ex(Q.make_config(variant=5, tile_m=16)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=5, split_k=33)) == Q.QUICK_ERR_INVALID_ARG  # more slices than k-groups
     assert ex(Q.make_config(variant=5), M=1, N=16 * 8 * 4097, K=128) == Q.QUICK_ERR_INVALID_ARG  # counters
-    assert ex(Q.make_config(variant=4), M=17) == Q.QUICK_ERR_INVALID_ARG       # more than 16 rows
-    assert ex(Q.make_config(variant=4), M=16, K=8192) == Q.QUICK_ERR_INVALID_ARG  # x over 128 KiB
-    assert ex(Q.make_config(variant=4), K=4224) == Q.QUICK_ERR_INVALID_ARG   # K/128 not a multiple of 16
-    assert ex(Q.make_config(variant=4, tile_n=1)) == Q.QUICK_ERR_INVALID_ARG
-    assert ex(Q.make_config(variant=4, split_k=513)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=4), M=1) == Q.QUICK_ERR_INVALID_ARG       # reserved number
+    assert ex(Q.make_config(variant=4), M=0) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=3, split_k=12)) == Q.QUICK_ERR_INVALID_ARG   # not a multiple of 8
     assert ex(Q.make_config(variant=3, split_k=8192)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=3, tile_m=128, tile_n=64)) == Q.QUICK_ERR_INVALID_ARG
@@ -138,11 +135,8 @@ def test_gemm_ex_validation_without_device():
     # more workgroups than (tile, k-group) units: clamped to the units (2 x 16 x 32 = 1024)
     sk = Q.make_config(variant=3, tile_m=128, tile_n=32, split_k=4096)
     assert Q.workspace_bytes(256, 4096, 4096, sk) == Q.WS_COUNTER_BYTES + 2 * 1024 * 128 * 256 * 4
-    # balanced stream kernel: counters, then two 1 KiB partial slots per wave
-    assert Q.workspace_bytes(1, 8192, 8192, Q.make_config(variant=4, split_k=256)) == \
-        Q.WS_COUNTER_BYTES + 2 * 256 * 8 * 1024
-    # no more waves than trips of 16 units (2 x 16 units = 2 trips: one workgroup)
-    assert Q.workspace_bytes(1, 32, 2048, Q.make_config(variant=4, split_k=64)) == Q.WS_COUNTER_BYTES + 2 * 8 * 1024
+    # the reserved variant number: no plan, no workspace
+    assert Q.workspace_bytes(1, 8192, 8192, Q.make_config(variant=4)) == 0
     # sliced stream kernel: counters, then 8 waves x n-tiles per wave x 1 KiB
     # per (column group, slice); slices raised to ceil(K/2048); one slice
     # needs none

@@ -71,32 +71,17 @@ def test_streamk_variants(M, cfg):
         _check(M, K, N, cfg, seed=M * 1000 + K + N + 11)
 
 
-# balanced stream kernel: G workgroups of 8 waves (0 = one per compute unit);
-# few workgroups make long ranges, many make ranges shorter than a tile
-BSTREAM_CFGS = [dict(variant=4, split_k=g) for g in (1, 3, 40, 0)]
-
-
-@pytest.mark.parametrize("cfg", BSTREAM_CFGS, ids=lambda c: "g%d" % c["split_k"])
-@pytest.mark.parametrize("M", [1, 3, 8, 16])
-def test_bstream_variants(M, cfg):
-    # K a multiple of 2048 (16 k-groups per ring trip); n-tiles of 1, 2, 3
-    # trips; x staged in LDS (at most 128 KiB)
-    for K, N in ((2048, 48), (4096, 272), (6144, 80), (2048, 16)):
-        if M * K * 2 <= 128 * 1024:
-            _check(M, K, N, cfg, seed=M * 1000 + K + N + 13)
-
-
-def test_bstream_deterministic_and_caller_workspace():
-    """Pieces summed in k order: repeated calls give identical bits, with
+def test_kstream_deterministic_and_caller_workspace():
+    """Slices summed in slice order: repeated calls give identical bits, with
     the internal or a caller workspace, whose counters are left zero."""
     M, K, N = 3, 8192, 528
     x, q, z, s = rand_case(77, M, K, N)
     p = Packed(q, z, s)
     xd = to_dev_x(x)
-    cfg = Q.make_config(variant=4, split_k=5)
+    cfg = Q.make_config(variant=5, split_k=5, tile_n=1)
     nb = Q.workspace_bytes(M, N, K, cfg)
     ws = torch.zeros(nb // 4 + 1, dtype=torch.int32, device="cuda")
-    say("bstream determinism ws=%d" % nb)
+    say("kstream determinism ws=%d" % nb)
     y0 = from_dev_y(p.gemm(xd, cfg=cfg))
     y1 = from_dev_y(p.gemm(xd, cfg=cfg, workspace=ws))
     y2 = from_dev_y(p.gemm(xd, cfg=cfg, workspace=ws))
@@ -139,13 +124,13 @@ def test_c1_toy_full_output():
 
 
 @pytest.mark.parametrize("cfg", [None, dict(variant=1, split_k=4, tile_n=2), dict(variant=2, tile_m=64, tile_n=32, split_k=2),
-                                 dict(variant=2, tile_m=128, tile_n=32, split_k=1), dict(variant=4, split_k=3),
+                                 dict(variant=2, tile_m=128, tile_n=32, split_k=1),
                                  dict(variant=5, split_k=3, tile_n=1), dict(variant=5, split_k=1, tile_n=2)])
 def test_one_hot_rows_give_exact_dequant(cfg):
     """x row m = e_{k_m}: y[m][n] is a single product, so it must equal the
     binary16 rounding of (q - z) * s exactly."""
-    K, N = (2048 if cfg and cfg["variant"] == 4 else 512), 96
-    M = 16 if cfg is None or cfg["variant"] in (1, 4, 5) else 100
+    K, N = 512, 96
+    M = 16 if cfg is None or cfg["variant"] in (1, 5) else 100
     g = np.random.Generator(np.random.PCG64(5))
     _, q, z, s = rand_case(6, 1, K, N)
     ks = g.choice(K, size=M, replace=False)
@@ -160,13 +145,12 @@ def test_one_hot_rows_give_exact_dequant(cfg):
 KSTREAM_EXACT = [dict(variant=5, split_k=1, tile_n=2), dict(variant=5, split_k=5, tile_n=1)]
 
 
-@pytest.mark.parametrize("cfg", [None] + STREAM_CFGS[::3] + TILED_CFGS[::3] + STREAMK_CFGS[::4] + BSTREAM_CFGS +
-                         KSTREAM_EXACT)
+@pytest.mark.parametrize("cfg", [None] + STREAM_CFGS[::3] + TILED_CFGS[::3] + STREAMK_CFGS[::4] + KSTREAM_EXACT)
 def test_integer_data_exact_under_any_split(cfg):
     """s = 1, z = 8, q in {7,8,9}, x in {-1,0,1}: every partial sum is a small
     integer, so any summation order is exact and y equals int64 x . (q - z)."""
-    M = 48 if cfg is None or cfg["variant"] == 1 else 16 if cfg["variant"] in (4, 5) else 150
-    K, N = (2048 if cfg and cfg["variant"] == 4 else 1024), 80
+    M = 48 if cfg is None or cfg["variant"] == 1 else 16 if cfg["variant"] == 5 else 150
+    K, N = 1024, 80
     g = np.random.Generator(np.random.PCG64(9))
     xi = g.integers(-1, 2, (M, K))
     qi = g.integers(7, 10, (K, N))
@@ -275,11 +259,11 @@ def test_m_zero_is_noop():
     p = Packed(q, z, s)
     y = p.gemm(torch.empty((0, K), dtype=torch.float16, device="cuda"))
     assert tuple(y.shape) == (0, N)
-    # every explicit kernel choice (K a multiple of 2048 for the balanced stream kernel)
+    # every explicit kernel choice
     K = 2048
     _, q, z, s = rand_case(2, 1, K, N)
     p = Packed(q, z, s)
-    for cfg in (dict(variant=1), dict(variant=4), dict(variant=5, split_k=2), dict(variant=3, tile_m=16, tile_n=16),
+    for cfg in (dict(variant=1), dict(variant=5, split_k=2), dict(variant=3, tile_m=16, tile_n=16),
                 dict(variant=2, tile_m=128, tile_n=32, split_k=2)):
         y = p.gemm(torch.empty((0, K), dtype=torch.float16, device="cuda"), cfg=Q.make_config(**cfg))
         assert tuple(y.shape) == (0, N)

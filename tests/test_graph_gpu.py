@@ -13,8 +13,9 @@ import numpy as np
 import pytest
 import torch
 
+import oracle
 import paper_2402_10076_amd as Q
-from gpu_util import Packed, rand_case, to_dev_x
+from gpu_util import TOL, Packed, from_dev_y, rand_case, rel_err, to_dev_x
 
 pytestmark = pytest.mark.gpu
 
@@ -112,3 +113,72 @@ def test_graph_replay_grouped_and_fused():
         Q.grouped_gemm(x, offsets, dw, ds, dz, N, rows=rows, cfg=Q.make_config(variant=2, split_k=2, tile_m=32,
                                                                                tile_n=16))
         torch.cuda.synchronize()
+
+
+def test_capture_without_workspace_returns_status():
+    """A first call on a fresh stream under capture, whose plan needs the
+    internal workspace, returns QUICK_ERR_CAPTURE and enqueues nothing (no
+    allocation, clear or synchronization on the capturing stream); after
+    an eager warm-up the same call captures and replays.  A graph captured
+    earlier keeps working after a larger plan grows the stream's buffer
+    (the old buffer is retired, not freed)."""
+    side = torch.cuda.Stream()
+    M, K, N = 48, 1024, 528
+    x, q, z, s = rand_case(500, M, K, N)
+    p = Packed(q, z, s)
+    xd = to_dev_x(x)
+    cfg = Q.make_config(variant=2, tile_m=32, tile_n=16, split_k=2)   # split-K: workspace needed
+    assert Q.workspace_bytes(M, N, K, cfg) > 0
+    y = torch.full((M, N), 7.0, dtype=torch.float16, device="cuda")
+    marker = torch.zeros(4, device="cuda")
+    torch.cuda.synchronize()
+    g0 = torch.cuda.CUDAGraph()
+    status = None
+    with torch.cuda.graph(g0, stream=side):
+        marker.fill_(1.0)
+        try:
+            p.gemm(xd, cfg=cfg, y=y)
+        except Q.QuickError as e:
+            status = e.status
+    assert status == Q.QUICK_ERR_CAPTURE
+    g0.replay()
+    torch.cuda.synchronize()
+    assert bool((marker == 1.0).all()) and bool((y == 7.0).all()), "the refused call left work in the graph"
+
+    with torch.cuda.stream(side):
+        p.gemm(xd, cfg=cfg, y=y)
+    side.synchronize()
+    eager = y.clone()
+    g1 = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g1, stream=side):
+        p.gemm(xd, cfg=cfg, y=y)
+    y.fill_(float("nan"))
+    torch.cuda.synchronize()
+    g1.replay()
+    torch.cuda.synchronize()
+    assert torch.equal(y, eager)
+
+    # a larger plan on the same stream: refused under capture, grows the
+    # buffer eagerly; the graph captured with the old buffer still replays
+    big = Q.make_config(variant=2, tile_m=32, tile_n=16, split_k=8)
+    assert Q.workspace_bytes(M, N, K, big) > Q.workspace_bytes(M, N, K, cfg)
+    yb = torch.empty_like(y)
+    g2 = torch.cuda.CUDAGraph()
+    status = None
+    with torch.cuda.graph(g2, stream=side):
+        marker.fill_(2.0)
+        try:
+            p.gemm(xd, cfg=big, y=yb)
+        except Q.QuickError as e:
+            status = e.status
+    assert status == Q.QUICK_ERR_CAPTURE
+    with torch.cuda.stream(side):
+        p.gemm(xd, cfg=big, y=yb)
+    side.synchronize()
+    assert rel_err(from_dev_y(yb), oracle.gemm(x, q, z, s)) <= TOL
+    for _ in range(3):
+        y.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g1.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y, eager)

@@ -167,41 +167,6 @@ def test_grouped_tile_table_clamps_malformed_offsets():
             assert 0 <= m0 < mend <= R
 
 
-def bstream_ranges(U, D, W):
-    UD = U // D
-    W = min(W, UD)
-    return W, [(w * UD // W * D, (w + 1) * UD // W * D) for w in range(W)]
-
-
-@pytest.mark.parametrize("NT,KG,G", [(3, 16, 1), (17, 32, 1), (5, 48, 3), (3584, 64, 256), (512, 224, 256),
-                                      (640, 64, 512), (2, 16, 64)])
-def test_bstream_ranges_pieces_and_slots(NT, KG, G):
-    D = 16
-    U = NT * KG
-    W, ranges = bstream_ranges(U, D, G * 8)
-    UD = U // D
-    covered = np.zeros(U, np.int64)
-    slots = {}
-    for gw, (u0, u1) in enumerate(ranges):
-        assert u1 > u0 and u0 % D == 0 and u1 % D == 0
-        covered[u0:u1] += 1
-        nt, pstart = u0 // KG, u0
-        for u in range(u0, u1):
-            if u % KG == KG - 1 or u == u1 - 1:
-                if not (pstart == nt * KG and u == nt * KG + KG - 1):
-                    slots[(nt, gw)] = 2 * gw + (0 if pstart == u0 else 1)
-                pstart = u + 1
-                if u % KG == KG - 1:
-                    nt += 1
-    assert np.all(covered == 1)
-    for (t, gw), slot in slots.items():
-        tb = t * KG
-        w0 = ((tb // D + 1) * W - 1) // UD
-        w1 = (((tb + KG - 1) // D + 1) * W - 1) // UD
-        assert w0 <= gw <= w1 < W
-        assert slot == 2 * gw + (0 if (gw * UD // W) * D >= tb else 1)
-
-
 def kstream_partition(M, N, K, npw, split):
     """Sliced stream kernel: the host's slice count and grid, then, per
     workgroup id, the kernel's (slice, column group), its waves' n-tiles and
