@@ -123,7 +123,7 @@ def test_capture_without_workspace_returns_status():
     earlier keeps working after a larger plan grows the stream's buffer
     (the old buffer is retired, not freed)."""
     side = torch.cuda.Stream()
-    M, K, N = 48, 1024, 528
+    M, K, N = 48, 1024, 2048
     x, q, z, s = rand_case(500, M, K, N)
     p = Packed(q, z, s)
     xd = to_dev_x(x)
@@ -161,7 +161,8 @@ def test_capture_without_workspace_returns_status():
     # a larger plan on the same stream: refused under capture, grows the
     # buffer eagerly; the graph captured with the old buffer still replays
     big = Q.make_config(variant=2, tile_m=32, tile_n=16, split_k=8)
-    assert Q.workspace_bytes(M, N, K, big) > Q.workspace_bytes(M, N, K, cfg)
+    # more than the first allocation (at least 1 MiB) holds
+    assert Q.workspace_bytes(M, N, K, big) > max(Q.workspace_bytes(M, N, K, cfg), 1 << 20)
     yb = torch.empty_like(y)
     g2 = torch.cuda.CUDAGraph()
     status = None
