@@ -164,6 +164,29 @@ int quick_w4a16_gemm_ex(const void* x, const void* packed, const void* scales,
                         int64_t group, void* stream, const quick_config_t* cfg,
                         void* workspace, size_t workspace_bytes);
 
+/* ---- allocation-free variant ----------------------------------------
+ * For callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, automatic kernel choice (including a loaded tune table) and
+ * results as quick_w4a16_gemm, but the split-K / stream-K / sliced-kernel
+ * workspace is a fixed library array of QUICK_SCRATCH_BYTES per GPU (a
+ * static device array, held on every GPU the library runs on until the
+ * process ends) instead of an allocation: the call itself never allocates,
+ * frees or synchronizes.  The first call on a device looks the array up and
+ * enqueues one small kernel on `stream` that zeroes its arrival counters
+ * (every GEMM leaves them zero again).
+ * All calls on one GPU share that GPU's array, which keeps the last call's
+ * contents: calls that may run at the same time on one GPU (different
+ * streams, or graph replays that overlap other such calls) race and give
+ * wrong results.  Order them on one stream.
+ * Errors: as quick_w4a16_gemm (no CAPTURE: nothing is allocated), plus
+ * WORKSPACE when the shape's plan needs more than QUICK_SCRATCH_BYTES
+ * (quick_workspace_bytes(M, N, K, NULL) tells beforehand). */
+#define QUICK_SCRATCH_BYTES ((size_t)80 << 20)
+int quick_w4a16_gemm_noalloc(const void* x, const void* packed, const void* scales,
+                             const void* zeros, void* y, int64_t M, int64_t N, int64_t K,
+                             int64_t group, void* stream);
+
 /* Workspace bytes quick_w4a16_gemm_ex needs for this shape and config
  * (cfg NULL = automatic choice); 0 when no workspace is used. */
 size_t quick_workspace_bytes(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg);

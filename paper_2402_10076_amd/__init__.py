@@ -54,6 +54,8 @@ _DEVICE_TYPE = "cuda"
 
 # leading workspace bytes that hold stream-K arrival counters (QUICK_WORKSPACE_COUNTER_BYTES)
 WS_COUNTER_BYTES = 16384
+# bytes of the per-GPU scratch array of quick_w4a16_gemm_noalloc (QUICK_SCRATCH_BYTES)
+SCRATCH_BYTES = 80 << 20
 
 _lock = threading.Lock()
 _lib = None
@@ -108,6 +110,8 @@ def lib():
             L.quick_w4a16_gemm_ex.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P,
                                               ctypes.POINTER(QuickConfig), P, SZ]
             L.quick_w4a16_gemm_ex.restype = I
+            L.quick_w4a16_gemm_noalloc.argtypes = [P, P, P, P, P, I64, I64, I64, I64, P]
+            L.quick_w4a16_gemm_noalloc.restype = I
             L.quick_workspace_bytes.argtypes = [I64, I64, I64, ctypes.POINTER(QuickConfig)]
             L.quick_workspace_bytes.restype = SZ
             L.quick_select_config.argtypes = [I64, I64, I64, ctypes.POINTER(QuickConfig)]
@@ -329,6 +333,24 @@ def w4a16_gemm(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zero
     return y
 
 
+def w4a16_gemm_noalloc(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor,
+                       N: int, y: torch.Tensor, group: int = 128, stream=None) -> torch.Tensor:
+    """quick_w4a16_gemm_noalloc: y = x . W with the library's fixed per-GPU
+    scratch array as workspace (no allocation in the call; y must be given).
+    Calls that may overlap on one GPU race on that array."""
+    what = "w4a16_gemm_noalloc"
+    _check_x(what, x)
+    M, K = x.shape
+    _check_weights(what, x, packed, scales, zeros, K, N, group)
+    if y is None:
+        raise QuickError(QUICK_ERR_INVALID_ARG, "%s: y must be given (the call allocates nothing)" % what)
+    y = _out(what, y, x, M, N)
+    hs = _stream(stream, x)
+    _check(lib().quick_w4a16_gemm_noalloc(_dptr(x), _dptr(packed), _dptr(scales), _dptr(zeros), _dptr(y),
+                                          M, N, K, group, hs), "quick_w4a16_gemm_noalloc")
+    return y
+
+
 def tune(x: torch.Tensor, packed: torch.Tensor, scales: torch.Tensor, zeros: torch.Tensor, N: int,
          y: torch.Tensor | None = None, group: int = 128, stream=None) -> dict:
     """Time every configuration for this shape on these buffers and record the
@@ -519,7 +541,8 @@ def tune_table_clear() -> None:
 
 EXPORTED = (
     "quick_status_string", "quick_pack_format_version", "quick_packed_sizes", "quick_pack_weights",
-    "quick_unpack_weights", "quick_w4a16_gemm", "quick_w4a16_gemm_ex", "quick_workspace_bytes",
+    "quick_unpack_weights", "quick_w4a16_gemm", "quick_w4a16_gemm_ex", "quick_w4a16_gemm_noalloc",
+    "quick_workspace_bytes",
     "quick_select_config", "quick_tune", "quick_tune_table_save", "quick_tune_table_load",
     "quick_tune_table_size", "quick_tune_table_clear", "quick_ablation_gemm",
     "quick_w4a16_grouped_gemm", "quick_w4a16_grouped_gemm_ex", "quick_grouped_workspace_bytes",

@@ -2002,6 +2002,74 @@ extern "C" int quick_w4a16_gemm_ex(const void* x, const void* packed, const void
                      workspace_bytes);
 }
 
+// ---------------------------------------------------------------------------
+// Allocation-free entry point (declared in quick.h): the workspace is this
+// file-scope device array, QUICK_SCRATCH_BYTES on every GPU the library runs
+// on, held until the process ends.  In host code its name only stands in
+// for the symbol: its device address comes from hipGetSymbolAddress, once per
+// device, with that device current.
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) uint8_t scratch[QUICK_SCRATCH_BYTES];
+
+namespace {
+
+__global__ void __launch_bounds__(256) scratch_clear_kernel(uint32_t* p, int n)
+{
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0u;
+}
+
+std::mutex g_scratch_mu;
+std::map<int, void*> g_scratch;  // device -> address of its copy of `scratch`
+
+// This device's scratch address; the first call on a device looks it up and
+// clears the arrival counters at its start with a kernel on `stream` (a
+// kernel rather than a memset node, so a capturing caller may take it into
+// its graph).  Every GEMM leaves the counters zero again.
+int scratch_address(hipStream_t stream, void** out)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return QUICK_ERR_HIP;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    const auto it = g_scratch.find(dev);
+    if (it != g_scratch.end()) {
+        *out = it->second;
+        return QUICK_OK;
+    }
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) {
+        (void)hipGetLastError();
+        return QUICK_ERR_HIP;
+    }
+    const int n = (int)(kSkCounterBytes / sizeof(uint32_t));
+    (void)hipGetLastError();
+    hipLaunchKernelGGL(scratch_clear_kernel, dim3((n + 255) / 256), dim3(256), 0, stream, static_cast<uint32_t*>(p),
+                       n);
+    if (hipGetLastError() != hipSuccess) return QUICK_ERR_HIP;
+    g_scratch[dev] = p;
+    *out = p;
+    return QUICK_OK;
+}
+
+}  // namespace
+
+extern "C" int quick_w4a16_gemm_noalloc(const void* x, const void* packed, const void* scales, const void* zeros,
+                                        void* y, int64_t M, int64_t N, int64_t K, int64_t group, void* stream)
+{
+    // argument errors are reported before any set-up
+    int st = validate(x, packed, scales, zeros, y, M, N, K, group);
+    if (st || M == 0) return st;
+    Plan pl;
+    st = make_plan(M, N, K, nullptr, &pl);
+    if (st) return st;
+    finish_plan(M, N, K, &pl);
+    if (plan_workspace(M, N, pl) > (size_t)QUICK_SCRATCH_BYTES) return QUICK_ERR_WORKSPACE;
+    void* ws = nullptr;
+    st = scratch_address((hipStream_t)stream, &ws);
+    if (st) return st;
+    return gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, nullptr, ws, (size_t)QUICK_SCRATCH_BYTES);
+}
+
 extern "C" size_t quick_workspace_bytes(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg)
 {
     if (M <= 0 || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return 0;

@@ -99,6 +99,34 @@ def test_gemm_validation_without_device():
     assert _gemm(**ok, M=4, N=1 << 20, K=1 << 17) == Q.QUICK_ERR_SHAPE
 
 
+def test_noalloc_validation_without_device(tmp_path):
+    """The allocation-free entry point reports argument errors, and a plan
+    larger than its fixed scratch array, before any device work."""
+    A = 0x10000
+    L = Q.lib()
+
+    def na(x=A, pw=A, ps=A, pz=A, y=A, M=4, N=4096, K=4096, group=128):
+        return L.quick_w4a16_gemm_noalloc(x, pw, ps, pz, y, M, N, K, group, None)
+    assert na(M=0) == Q.QUICK_OK
+    assert na(M=-1) == Q.QUICK_ERR_SHAPE
+    assert na(K=4000) == Q.QUICK_ERR_SHAPE
+    assert na(group=64) == Q.QUICK_ERR_UNSUPPORTED
+    assert na(x=0) == Q.QUICK_ERR_INVALID_ARG
+    assert na(y=A + 4) == Q.QUICK_ERR_ALIGNMENT
+    # every automatic plan of the benchmark shapes fits the scratch array
+    for M, N, K in ((1024, 10240, 8192), (512, 57344, 8192), (128, 8192, 28672), (16, 12288, 4096)):
+        assert 0 <= Q.workspace_bytes(M, N, K) <= Q.SCRATCH_BYTES
+    # a tuned plan whose partial sums exceed it is refused
+    big = tmp_path / "big.txt"
+    big.write_text("quick-tune 1\n1024 57344 8192 2 8 128 32\n")
+    Q.tune_table_load(str(big))
+    try:
+        assert Q.workspace_bytes(1024, 57344, 8192) > Q.SCRATCH_BYTES
+        assert na(M=1024, N=57344, K=8192) == Q.QUICK_ERR_WORKSPACE
+    finally:
+        Q.tune_table_clear()
+
+
 def test_gemm_ex_validation_without_device():
     A = 0x10000
     L = Q.lib()
