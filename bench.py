@@ -333,6 +333,52 @@ def copy_calibration():
     log("copy calibration: 5 x %d MiB device copies" % (COPY_CAL_BYTES >> 20))
 
 
+READ_CEILING_MB = (4.4, 8.7, 17.4, 23.4, 26.2, 34.9, 43.6, 46.9, 65.9, 122.0, 244.0)
+
+
+def read_ceiling(sizes_mb=READ_CEILING_MB, reps=40):
+    """The practical ceiling of short HBM transfers: device-to-device copies
+    (torch, the HIP runtime's copy kernel) of the packed-weight sizes of the
+    benchmark GEMMs, each copy rotating through sources and destinations
+    spanning >= 1 GiB (so every copy streams from HBM, not the Infinity
+    Cache), `reps` copies captured in a graph and timed with HIP events
+    around replays.  Returns per size the copy time and the read rate (bytes
+    read / time) and read + write rate."""
+    import torch
+    rows = []
+    st = torch.cuda.Stream()
+    for mb in sizes_mb:
+        n = int(mb * 1e6) // 16 * 16
+        k = max(2, -(-(1 << 30) // n))
+        src = [torch.empty(n, dtype=torch.uint8, device="cuda") for _ in range(k)]
+        dst = [torch.empty(n, dtype=torch.uint8, device="cuda") for _ in range(k)]
+        for t in src:
+            t.fill_(1)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=st):
+            for r in range(reps):
+                dst[r % k].copy_(src[(r + 1) % k])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        best = None
+        with torch.cuda.stream(st):
+            g.replay()
+            for _ in range(5):
+                e0.record()
+                g.replay()
+                e1.record()
+                e1.synchronize()
+                us = e0.elapsed_time(e1) / reps * 1e3
+                best = us if best is None else min(best, us)
+        rows.append(dict(mb=mb, bytes=n, copies_rotated=k, us=round(best, 2),
+                         read_gbs=round(n / best / 1e3, 1), read_write_gbs=round(2 * n / best / 1e3, 1)))
+        log("read ceiling %7.1f MB: %8.2f us, read %7.1f GB/s, read+write %7.1f GB/s" % (
+            mb, best, n / best / 1e3, 2 * n / best / 1e3))
+        del g, src, dst
+        torch.cuda.empty_cache()
+    return rows
+
+
 def compare_fp16(K, N, Ms, reps=20):
     """Context only: the W4A16 GEMM beside an fp16 GEMM of the same shape
     through torch (hipBLASLt) on the dequantized weights, each timed with HIP
@@ -625,6 +671,9 @@ def main():
     ap.add_argument("--dominant", default="",
                     help="kernel name for --ingest-pmc/--ingest-trace (default: the dominant kernel of the "
                          "--points-out file of the profiled bench run)")
+    ap.add_argument("--read-ceiling", action="store_true",
+                    help="only time device-to-device copies of the benchmark's weight sizes (HBM ceiling of "
+                         "short transfers, context for the M <= 16 roofline)")
     ap.add_argument("--compare-fp16", action="store_true",
                     help="only compare the W4A16 GEMM with an fp16 GEMM through torch (hipBLASLt) on the "
                          "8192x8192 Llama-2-70B o_proj shape over M (context, not the metric)")
@@ -726,6 +775,10 @@ def main():
         return
     if args.moe:
         print(json.dumps({"moe": "Mixtral-8x7B expert FFN, dense per expert vs grouped", **moe(sweep=not args.moe_auto_only)}))
+        return
+    if args.read_ceiling:
+        print(json.dumps({"read_ceiling": "device-to-device copies rotating >= 1 GiB, graph of 40",
+                          "rows": read_ceiling()}))
         return
     if args.compare_fp16:
         rows = compare_fp16(8192, 8192, [1, 4, 16, 32, 64, 128, 256, 512, 1024, 2048])
