@@ -51,8 +51,8 @@ def kernel_name(sel: dict) -> str:
         return "stream_kernel<MT,%d,%d>" % (sel["tile_n"], sel["split_k"])
     if sel["variant"] == 5:
         return "kstream_kernel<%d>(S=%d)" % (sel["tile_n"], sel["split_k"])
-    name = "tiled_kernel<%d,%d>" % (sel["tile_m"], sel["tile_n"])
-    if sel["variant"] == 3:
+    name = "tiled%s_kernel<%d,%d>" % ("32" if sel["variant"] in (6, 7) else "", sel["tile_m"], sel["tile_n"])
+    if sel["variant"] in (3, 7):
         name += "+streamK(G=%d)" % sel["split_k"]
     elif sel["split_k"] > 1:
         name += "+splitk_reduce(S=%d)" % sel["split_k"]
@@ -75,6 +75,10 @@ def launch_sequence(points):
             seq.append((p["kernel"], "stream_kernel<"))
         elif sel["variant"] == 5:
             seq.append((p["kernel"], "kstream_kernel<%d>" % sel["tile_n"]))
+        elif sel["variant"] in (6, 7):
+            seq.append((p["kernel"], "tiled32_kernel<%d, %d, false>" % (sel["tile_m"], sel["tile_n"])))
+            if sel["variant"] == 6 and sel["split_k"] > 1:
+                seq.append((None, "splitk_reduce_kernel"))
         else:
             seq.append((p["kernel"], "tiled_kernel<%d, %d, 0, false, false>" % (sel["tile_m"], sel["tile_n"])))
             if sel["variant"] == 2 and sel["split_k"] > 1:
@@ -181,7 +185,7 @@ def ingest_trace(trace_csv, points, dominant, out_md, command, run_log=""):
     j = 0
     for rep in range(reps):
         for i, p in enumerate(points):
-            n = 2 if (p["sel"]["variant"] == 2 and p["sel"]["split_k"] > 1) else 1
+            n = 2 if (p["sel"]["variant"] in (2, 6) and p["sel"]["split_k"] > 1) else 1
             for t in range(n):
                 per_point[i][rep] += rows[j + t][2]
             if p["kernel"] == dominant:
@@ -283,7 +287,7 @@ def ingest_mfma(csv_path, points, out_md, command):
             d = disp[ids[j]]   # the GEMM kernel itself (a split-K reduction follows it)
             for c in MFMA_COUNTERS:
                 acc[i].setdefault(c, []).append(d.get(c, 0.0))
-            j += 2 if (p["sel"]["variant"] == 2 and p["sel"]["split_k"] > 1) else 1
+            j += 2 if (p["sel"]["variant"] in (2, 6) and p["sel"]["split_k"] > 1) else 1
     lines = ["| cfg | shape | K | N | M | kernel | matrix busy % | matrix flops / algorithmic | LDS instr | LDS bank conflicts |",
              "|---|---|---|---|---|---|---|---|---|---|"]
     for i, p in enumerate(points):

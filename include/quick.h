@@ -129,17 +129,21 @@ typedef struct quick_config {
                       5 = sliced stream kernel (M <= 16: the 8 waves of a
                       workgroup split 128 or 256 columns, workgroups split
                       K into slices of at most 2048 channels whose rows of x
-                      they stage in LDS once; N/128 <= 4096)                */
-    int split_k;   /* variant 2: K slices across workgroups; variant 1: waves
-                      per workgroup (1, 2, 4, 8); variant 3: resident
+                      they stage in LDS once; N/128 <= 4096),
+                      6 = tiled kernel on the 32x32x16 matrix instruction
+                      (waves of 32 columns: two n-tiles per instruction),
+                      7 = the same with the stream-K schedule              */
+    int split_k;   /* variants 2, 6: K slices across workgroups; variant 1:
+                      waves per workgroup (1, 2, 4, 8); variants 3, 7: resident
                       workgroups, a multiple of 8 up to 4096 (clamped to the
                       number of tile x 128-channel units); variant 5: K
                       slices (raised to at least
                       ceil(K/2048), at most K/128); 0 = auto                */
     int tile_m;    /* tiled kernel rows per workgroup: 16, 32, 64 or 128
                       (variant 5: must be 0);
-                      supported (tile_m, tile_n) pairs: (16|32, 16|32),
-                      (64, 32), (64, 64), (128, 32)                         */
+                      supported (tile_m, tile_n) pairs, variants 2, 3:
+                      (16|32|64|128, 16|32), (64, 64); variants 6, 7:
+                      (32|64|128, 32)                                        */
     int tile_n;    /* tiled kernel columns per wave: 16, 32 or 64
                       stream kernels (variants 1, 5): n-tiles per wave: 1 or
                       2                                                      */
@@ -200,10 +204,13 @@ int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config_t* cfg);
 
 /* Times every supported kernel configuration for this shape on the caller's
  * buffers (same arguments and contract as quick_w4a16_gemm; y is
- * overwritten, the last write coming from the best configuration) with HIP
- * events on `stream` (per configuration the fastest of three timings of
- * max(10, copies) launches), and records the fastest in the process-wide tune
- * table, keyed by (M, N, K).  From then on quick_w4a16_gemm, and the
+ * overwritten, the last write coming from the best configuration) and
+ * records the fastest in the process-wide tune table.  Each configuration's
+ * max(20, copies) launches are captured as one HIP graph on a private
+ * stream (which first waits for `stream`) and timed with HIP events as the
+ * fastest of three replays, so the host's per-launch cost does not enter
+ * the timing of short kernels.  The table is keyed by (M, N, K).  From
+ * then on quick_w4a16_gemm, and the
  * automatic choice of quick_w4a16_gemm_ex / quick_workspace_bytes /
  * quick_select_config, use the recorded configuration for that shape on
  * every device.  The timed launches rotate through temporary device copies
@@ -211,11 +218,12 @@ int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config_t* cfg);
  * Infinity Cache, at most 64 copies), so that each launch streams its
  * weights from HBM as in a forward pass; when that memory cannot be
  * allocated, they repeat the caller's buffers.
- * Blocking: synchronizes `stream`; takes tens of milliseconds to a few
- * hundred; allocates and frees the copies and may grow the internal
- * workspace, so not for use under graph capture.  `best` (may be NULL) receives the
+ * Blocking: waits for its own work; takes tens of milliseconds to a few
+ * hundred; allocates and frees the copies and allocates a workspace for its
+ * private stream (kept until process exit), so not for use under graph
+ * capture (QUICK_ERR_CAPTURE when `stream` is capturing).  `best` (may be NULL) receives the
  * configuration recorded.  M == 0 records nothing.
- * Errors: as quick_w4a16_gemm. */
+ * Errors: as quick_w4a16_gemm, plus CAPTURE. */
 int quick_tune(const void* x, const void* packed, const void* scales, const void* zeros, void* y,
                int64_t M, int64_t N, int64_t K, int64_t group, void* stream, quick_config_t* best);
 

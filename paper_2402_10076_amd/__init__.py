@@ -47,6 +47,8 @@ VARIANT_STREAM = 1
 VARIANT_TILED = 2
 VARIANT_STREAMK = 3
 VARIANT_KSTREAM = 5
+VARIANT_TILED32 = 6
+VARIANT_STREAMK32 = 7
 
 # torch device type of every tensor whose address goes to the library (the
 # CPU tests of the argument checks substitute "meta")

@@ -1297,6 +1297,383 @@ kstream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
     if (threadIdx.x == 0) __hip_atomic_store(&counters[cg], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// ---------------------------------------------------------------------------
+// Tiled kernel on the 32x32x16 matrix instruction (large M).
+//
+// The tiles, schedules (data-parallel, split-K, stream-K with the
+// last-arriver fix-up), XCD-aware tile order and the 4-stage activation ring
+// in LDS are those of tiled_kernel.  What differs is the matrix step: each
+// wave multiplies pairs of n-tiles (32 output columns) with
+// v_mfma_f32_32x32x16_f16, one 32 x 16 weight operand against BM/32
+// activation operands of 32 rows per 16-channel step, so a k-group takes
+// half as many matrix instructions for the same fragment reads and the same
+// dequantization.
+//
+// The QPK16 units serve this operand without repacking.  Lane l of the
+// instruction holds output column l % 32 of the pair (n-tile t = (l/16) % 2,
+// column c = l % 16) and channels 8h .. 8h+7 (h = l / 32) of the step.  It
+// loads the 16 bytes of QPK16 lane 16h + c of n-tile t's unit, whose words
+// hold channels 32j + 8h + e, and those of QPK16 lane 16(h+2) + c, channels
+// 32j + 16 + 8h + e.  Step s = 2j (first load, word j) and s = 2j + 1
+// (second load, word j) then covers channels 16s + 8h + e for every row, the
+// k assignment the activation operand uses too: lane l reads row l % 32 of
+// its block, channel chunk 2s + h of the stage.
+//
+// Output: lane l holds row l % 32 of a block and, in accumulator 4b + i, the
+// column 8b + 4h + i of the pair, so every lane stores four 8-byte quads per
+// block (b = 0, 1 in the first n-tile, b = 2, 3 in the second).
+// ---------------------------------------------------------------------------
+typedef float f16v_t __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ f16v_t mfma32(const h8_t& a, const h8_t& b, const f16v_t& c)
+{
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+template <int BM, int WN, bool EP = false>
+__global__ void __launch_bounds__(64 * kTiledWaves, 1)
+tiled32_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
+               const uint16_t* __restrict__ ps, const uint32_t* __restrict__ pz,
+               uint16_t* __restrict__ y, float* __restrict__ ws, int M, int N, int K,
+               int kg_per_split, int n_mtiles, int n_ntiles, int n_splits, Epi epi)
+{
+    constexpr int WAVES = kTiledWaves;
+    constexpr int NST = kTiledStages;
+    constexpr int NPR = WN / 32;                  // n-tile pairs per wave
+    constexpr int NP = 2 * NPR;                   // n-tiles per wave
+    constexpr int MB = BM / 32;                   // 32-row blocks
+    constexpr int ROWB = 256;                     // bytes per activation row of a stage
+    constexpr int STAGE = BM * ROWB;
+    constexpr int NDMA = STAGE / 1024;            // 1 KiB LDS-DMA instructions per stage
+    constexpr int DMA_PER_WAVE = (NDMA + WAVES - 1) / WAVES;
+    static_assert(WN % 32 == 0 && BM % 32 == 0, "pairs of n-tiles and 32-row blocks");
+    static_assert(NDMA >= 1 && STAGE % 1024 == 0 && (NDMA % WAVES == 0 || NDMA < WAVES), "DMA split");
+    static_assert(2 * (DMA_PER_WAVE + 4 * NPR) < 64, "vmcnt range");
+    static_assert(NST == 4, "stage objects below");
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_s0[STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_s1[STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_s2[STAGE];
+    __shared__ __attribute__((aligned(1024))) uint8_t lds_s3[STAGE];
+    auto stage_ptr = [&](int st) -> uint8_t* {
+        return st == 0 ? lds_s0 : st == 1 ? lds_s1 : st == 2 ? lds_s2 : lds_s3;
+    };
+
+    const int KG = K >> 7;
+    const int NT = N >> 4;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int c = lane & 15;          // column inside the n-tile
+    const int tp = (lane >> 4) & 1;   // n-tile of the pair
+    const int h = lane >> 5;          // channel half of a 16-channel step
+    const int r32 = lane & 31;        // row inside a 32-row block
+
+    const size_t wbytes = (size_t)K * N / 2;
+    const rsrc_t rw = make_rsrc(pw, (uint32_t)wbytes);
+    const rsrc_t rs = make_rsrc(ps, (uint32_t)(wbytes / 32));
+    const rsrc_t rz = make_rsrc(pz, (uint32_t)(wbytes / 128));
+    const rsrc_t rx = make_rsrc(x, (uint32_t)((size_t)M * K * 2));
+    const int ndma = NDMA >= WAVES ? DMA_PER_WAVE : (wave < NDMA ? 1 : 0);
+
+    int m0 = 0;     // first row of the tile
+    int ntw = 0;    // first n-tile of this wave
+    // per pair: this lane's byte offsets of its n-tile's first unit (packed
+    // weights at its QPK16 lane 16h + c, scales, zeros); n-tiles past the
+    // end are clamped to the last one (computed, never stored)
+    uint32_t vw[NPR], vs[NPR], vz[NPR];
+    uint32_t vx[DMA_PER_WAVE];
+    auto set_tile = [&](int t) __attribute__((always_inline)) {
+        m0 = (t % n_mtiles) * BM;
+        const int ntile = (t / n_mtiles) % n_ntiles;
+        ntw = ntile * (WAVES * NP) + wave * NP;
+#pragma unroll
+        for (int pr = 0; pr < NPR; ++pr) {
+            const uint32_t u = (uint32_t)min(ntw + 2 * pr + tp, NT - 1) * (uint32_t)KG;
+            vw[pr] = u * 1024u + (uint32_t)(16 * h + c) * 16u;
+            vs[pr] = u * 32u + (uint32_t)c * 2u;
+            vz[pr] = u * 8u + (uint32_t)(c >> 3) * 4u;
+        }
+#pragma unroll
+        for (int i = 0; i < DMA_PER_WAVE; ++i) {
+            const int rr = (wave + i * WAVES) * 4 + (lane >> 4);
+            const int row = min(m0 + rr, M - 1);
+            vx[i] = ((uint32_t)row * (uint32_t)K + 8 * ((lane & 15) ^ (rr & 15))) * 2;
+        }
+    };
+
+    u4_t wa[NST][NPR], wb[NST][NPR];
+    uint32_t sr[NST][NPR], zr[NST][NPR];
+    auto fetch = [&](int st, int kg) __attribute__((always_inline)) {
+        const uint32_t soff = uniform((uint32_t)kg * 256u);
+#pragma unroll
+        for (int i = 0; i < DMA_PER_WAVE; ++i)
+            if (i < ndma) dma16(rx, stage_ptr(st) + (wave + i * WAVES) * 1024, vx[i], soff);
+#pragma unroll
+        for (int pr = 0; pr < NPR; ++pr) {
+            wa[st][pr] = ld128(rw, vw[pr], uniform((uint32_t)kg * 1024u));
+            wb[st][pr] = ld128(rw, vw[pr] + 512u, uniform((uint32_t)kg * 1024u));
+            sr[st][pr] = ld16(rs, vs[pr], uniform((uint32_t)kg * 32u));
+            zr[st][pr] = ld32(rz, vz[pr], uniform((uint32_t)kg * 8u));
+        }
+    };
+    auto wait_vmc = [](auto n) { __builtin_amdgcn_s_waitcnt(0x0F70 | (n & 15) | ((n >> 4) << 14)); };
+    constexpr int GL_FULL = DMA_PER_WAVE + 4 * NPR;
+    constexpr int GL_NODMA = 4 * NPR;
+    auto wait_groups = [&](int groups) {
+        if (ndma == DMA_PER_WAVE) {
+            if (groups >= 2) wait_vmc(std::integral_constant<int, 2 * GL_FULL>{});
+            else if (groups == 1) wait_vmc(std::integral_constant<int, GL_FULL>{});
+            else wait_vmc(std::integral_constant<int, 0>{});
+        } else {
+            if (groups >= 2) wait_vmc(std::integral_constant<int, 2 * GL_NODMA>{});
+            else if (groups == 1) wait_vmc(std::integral_constant<int, GL_NODMA>{});
+            else wait_vmc(std::integral_constant<int, 0>{});
+        }
+    };
+
+    f16v_t acc[NPR][MB];
+    // activation operand of step s: row mb*32 + r32, channel chunk 2s + h
+    // (stored at position (2s + h) ^ (row % 16), row % 16 == c)
+    auto bfrag = [&](int st, int mb, int s) -> h8_t {
+        const uint8_t* src = stage_ptr(st) + (mb * 32 + r32) * ROWB + (((2 * s + h) ^ c) << 4);
+        return bits_as<h8_t>(*reinterpret_cast<const u4_t*>(src));
+    };
+    Deq dcur[NPR];
+    auto make_d = [&](int st, Deq (&d)[NPR]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int pr = 0; pr < NPR; ++pr) d[pr] = make_deq(sr[st][pr], (zr[st][pr] >> (4 * (c & 7))) & 15u);
+    };
+    auto afrag = [&](int st, int pr, int s, const Deq (&d)[NPR]) -> h8_t {
+        return dequant8((s & 1) ? wb[st][pr][s >> 1] : wa[st][pr][s >> 1], d[pr]);
+    };
+    h8_t fa[2][NPR];
+    h8_t fb[2][MB];
+    auto load_step0 = [&](int st) __attribute__((always_inline)) {
+        make_d(st, dcur);
+#pragma unroll
+        for (int pr = 0; pr < NPR; ++pr) fa[0][pr] = afrag(st, pr, 0, dcur);
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) fb[0][mb] = bfrag(st, mb, 0);
+    };
+    // One k-group (8 steps of 16 channels) on stage / ring slot st, its
+    // step-0 operands already in fa[0], fb[0]; the operands of step s+1 are
+    // read and dequantized under the matrix instructions of step s, the
+    // last step's under those of the next k-group's first.
+    auto kgroup = [&](int st, int wgroups, bool next) __attribute__((always_inline)) {
+        const int sn = (st + 1) % NST;
+        Deq dn[NPR];
+#pragma unroll
+        for (int s = 0; s < 8; ++s) {
+            const int cu = s & 1, nx = cu ^ 1;
+            if (s == 7 && next) make_d(sn, dn);
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+                for (int pr = 0; pr < NPR; ++pr) acc[pr][mb] = mfma32(fa[cu][pr], fb[cu][mb], acc[pr][mb]);
+                if (s < 7) fb[nx][mb] = bfrag(st, mb, s + 1);
+                else if (next) fb[nx][mb] = bfrag(sn, mb, 0);
+            }
+            if (s < 7) {
+#pragma unroll
+                for (int pr = 0; pr < NPR; ++pr) fa[nx][pr] = afrag(st, pr, s + 1, dcur);
+            } else if (next) {
+#pragma unroll
+                for (int pr = 0; pr < NPR; ++pr) fa[nx][pr] = afrag(sn, pr, 0, dn);
+            }
+            constexpr int VPER = (13 * NPR + MB - 1) / MB;  // dequant VALU ops per block
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                __builtin_amdgcn_sched_group_barrier(0x008, NPR, 0);   // matrix
+                __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);     // LDS read
+                __builtin_amdgcn_sched_group_barrier(0x002, VPER, 0);  // VALU
+            }
+            if (s == 6) {
+                // k-group st+1 has landed for every wave, and every wave's
+                // reads of stage st have returned (see tiled_kernel)
+                wait_groups(wgroups);
+                wait_lds();
+                barrier();
+                sched_fence();
+            }
+        }
+        if (next) {
+#pragma unroll
+            for (int pr = 0; pr < NPR; ++pr) dcur[pr] = dn[pr];
+        }
+    };
+
+    auto run = [&](int kb, int ke) __attribute__((always_inline)) {
+#pragma unroll
+        for (int pr = 0; pr < NPR; ++pr)
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[pr][mb][v] = 0.f;
+#pragma unroll
+        for (int i = 0; i < NST - 1; ++i)
+            if (kb + i < ke) fetch(i, kb + i);
+        wait_groups(min(NST - 2, ke - kb - 1));
+        barrier();
+        sched_fence();
+        load_step0(0);
+        int kg = kb;
+        for (; kg + 2 * NST - 1 <= ke; kg += NST) {
+#pragma unroll
+            for (int i = 0; i < NST; ++i) {
+                fetch((i + NST - 1) % NST, kg + i + NST - 1);
+                kgroup(i, NST - 2, true);
+            }
+        }
+        for (; kg < ke; kg += NST) {
+#pragma unroll
+            for (int i = 0; i < NST; ++i) {
+                const int k = kg + i;
+                if (k < ke) {
+                    if (k + NST - 1 < ke) fetch((i + NST - 1) % NST, k + NST - 1);
+                    kgroup(i, min(NST - 2, ke - k - 2), k + 1 < ke);
+                }
+            }
+        }
+    };
+
+    // quad b (0..3) of block mb of pair pr: columns 16(ntw+2pr) + 8b + 4h .. +3
+    auto quad = [&](const f16v_t& v, int b) -> f4_t { return f4_t{v[4 * b], v[4 * b + 1], v[4 * b + 2], v[4 * b + 3]}; };
+    auto store_y = [&](const f16v_t (&v)[NPR][MB]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int pr = 0; pr < NPR; ++pr) {
+            const int nb = (ntw + 2 * pr) * 16 + 4 * h;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                const int m = m0 + mb * 32 + r32;
+                if (m >= M) continue;
+                if (EP && epi.act) {
+                    // gate quads b = 0, 1 with their up quads b + 2 (16 columns on)
+                    if (ntw + 2 * pr < NT) {
+                        store_gated(y, epi, m, N, nb, quad(v[pr][mb], 0), quad(v[pr][mb], 2));
+                        store_gated(y, epi, m, N, nb + 8, quad(v[pr][mb], 1), quad(v[pr][mb], 3));
+                    }
+                    continue;
+                }
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    if (ntw + 2 * pr + (b >> 1) >= NT) continue;
+                    if constexpr (EP) store_out(y, epi, m, N, nb + 8 * b, quad(v[pr][mb], b));
+                    else store_h4(y + (size_t)m * N + nb + 8 * b, quad(v[pr][mb], b));
+                }
+            }
+        }
+    };
+
+    if (n_splits > 0) {
+        // data-parallel / split-K: one (tile, K slice) per workgroup
+        const int nblk = n_mtiles * n_ntiles * n_splits;
+        const int per_xcd = gridDim.x >> 3;
+        const int t = (blockIdx.x & 7) * per_xcd + (blockIdx.x >> 3);
+        if (t >= nblk) return;
+        const int split = t / (n_mtiles * n_ntiles);
+        const int tin = t - split * (n_mtiles * n_ntiles);
+        set_tile(tin);
+        const int kb = split * kg_per_split;
+        run(kb, min(KG, kb + kg_per_split));
+        if (n_splits == 1) {
+            store_y(acc);
+            return;
+        }
+        float* part = ws + kSkCounterBytes / sizeof(float) + (size_t)split * M * N;
+#pragma unroll
+        for (int pr = 0; pr < NPR; ++pr) {
+            const int nb = (ntw + 2 * pr) * 16 + 4 * h;
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb) {
+                const int m = m0 + mb * 32 + r32;
+                if (m >= M) continue;
+#pragma unroll
+                for (int b = 0; b < 4; ++b)
+                    if (ntw + 2 * pr + (b >> 1) < NT)
+                        *reinterpret_cast<f4_t*>(part + (size_t)m * N + nb + 8 * b) = quad(acc[pr][mb], b);
+            }
+        }
+        return;
+    }
+
+    // ---- stream-K (see tiled_kernel): equal contiguous ranges of the
+    // tiles x k-groups units, last-arriver fix-up in k order
+    const int64_t U = (int64_t)n_mtiles * n_ntiles * KG;
+    const int G = gridDim.x;
+    const int wid = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+    const int64_t u0 = (int64_t)wid * U / G;
+    const int64_t u1 = (int64_t)(wid + 1) * U / G;
+    unsigned* counters = reinterpret_cast<unsigned*>(ws);
+    // partial-tile slot: thread-major f4 at (((wave * NPR + pr) * MB + mb) * 4 + b) * 64 + lane
+    constexpr uint32_t SLOT_BYTES = (uint32_t)WAVES * NPR * MB * 4 * 64 * 16;
+    const rsrc_t rp = make_rsrc(ws + kSkCounterBytes / sizeof(float), (uint32_t)(2 * gridDim.x) * SLOT_BYTES);
+    auto slot_off = [&](int pr, int mb, int b) -> uint32_t {
+        return (uint32_t)(((((wave * NPR + pr) * MB + mb) * 4 + b) * 64 + lane) * 16);
+    };
+    __shared__ int sk_last;
+    for (int64_t u = u0; u < u1;) {
+        const int tt = (int)(u / KG);
+        const int kb = (int)(u - (int64_t)tt * KG);
+        const int ke = (int)min<int64_t>(KG, kb + (u1 - u));
+        set_tile(tt);
+        run(kb, ke);
+        if (kb == 0 && ke == KG) {
+            store_y(acc);
+        } else {
+            const int64_t tb = (int64_t)tt * KG;
+            const int w0 = (int)(((tb + 1) * G - 1) / U);
+            const int w1 = (int)(((tb + KG) * G - 1) / U);
+            const uint32_t mine = uniform((uint32_t)(2 * wid + (u == u0 ? 0 : 1)) * SLOT_BYTES);
+#pragma unroll
+            for (int pr = 0; pr < NPR; ++pr)
+#pragma unroll
+                for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+                    for (int b = 0; b < 4; ++b)
+                        __builtin_amdgcn_raw_buffer_store_b128(bits_as<u4_t>(quad(acc[pr][mb], b)), rp,
+                                                               slot_off(pr, mb, b), mine, kCoherentAux);
+            wait_all();
+            __syncthreads();
+            if (threadIdx.x == 0)
+                sk_last = __hip_atomic_fetch_add(&counters[w1], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
+                          (unsigned)(w1 - w0);
+            __syncthreads();
+            if (sk_last) {
+#pragma unroll
+                for (int pr = 0; pr < NPR; ++pr) {
+#pragma unroll
+                    for (int mb = 0; mb < MB; ++mb) {
+#pragma unroll
+                        for (int b = 0; b < 4; ++b) {
+                            f4_t sum = f4_t{0.f, 0.f, 0.f, 0.f};
+                            for (int w = w0; w <= w1; ++w) {
+                                f4_t v;
+                                if (w == wid) {
+                                    v = quad(acc[pr][mb], b);
+                                } else {
+                                    const int first = (int64_t)w * U / G >= tb ? 0 : 1;
+                                    v = bits_as<f4_t>(__builtin_amdgcn_raw_buffer_load_b128(
+                                        rp, slot_off(pr, mb, b), uniform((uint32_t)(2 * w + first) * SLOT_BYTES),
+                                        kCoherentAux));
+                                }
+                                sum = w == w0 ? v : sum + v;
+                            }
+                            acc[pr][mb][4 * b] = sum[0];
+                            acc[pr][mb][4 * b + 1] = sum[1];
+                            acc[pr][mb][4 * b + 2] = sum[2];
+                            acc[pr][mb][4 * b + 3] = sum[3];
+                        }
+                    }
+                }
+                store_y(acc);
+                if (threadIdx.x == 0)
+                    __hip_atomic_store(&counters[w1], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+        }
+        u += ke - kb;
+        __syncthreads();  // LDS stages and sk_last are reused by the next piece
+    }
+}
+
 // Sum of S fp32 partial outputs [S][rows][N] in split order, then the
 // epilogue and one rounding to f16.  One thread per 4 output columns.
 __global__ void __launch_bounds__(256)
@@ -1332,6 +1709,8 @@ constexpr int kVariantStreamK = 3;  // tiled kernel, stream-K schedule
 // (variant 4, a balanced stream kernel, was withdrawn: it never won on a
 // measured shape; the number stays reserved and is rejected)
 constexpr int kVariantKStream = 5;  // sliced stream kernel
+constexpr int kVariantTiled32 = 6;   // tiled kernel on the 32x32x16 instruction
+constexpr int kVariantStreamK32 = 7; // the same, stream-K schedule
 
 int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
@@ -1340,7 +1719,13 @@ int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 int ks_groups(int64_t N, int npw) { return ceil_div(N / 16, kKsWaves * npw); }
 int ks_min_slices(int64_t K) { return ceil_div(K / 128, kKsMaxKg); }
 
-bool is_tiled(int variant) { return variant == kVariantTiled || variant == kVariantStreamK; }
+bool is_tiled(int variant)
+{
+    return variant == kVariantTiled || variant == kVariantStreamK || variant == kVariantTiled32 ||
+           variant == kVariantStreamK32;
+}
+bool is_streamk(int variant) { return variant == kVariantStreamK || variant == kVariantStreamK32; }
+bool is_t32(int variant) { return variant == kVariantTiled32 || variant == kVariantStreamK32; }
 
 // Bytes of one stream-K partial-tile slot.
 size_t sk_slot_bytes(int bm, int wn) { return (size_t)bm * kTiledWaves * wn * sizeof(float); }
@@ -1350,12 +1735,13 @@ size_t sk_slot_bytes(int bm, int wn) { return (size_t)bm * kTiledWaves * wn * si
 #if QUICK_TILED
 namespace quick {
 
-template <int BM, int WN>
-int tiled_resident_per_cu()
+template <class F>
+int resident_per_cu(F* kernel)
 {
     int n = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(&tiled_kernel<BM, WN>),
-                                                     64 * kTiledWaves, 0) != hipSuccess || n < 1)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(kernel), 64 * kTiledWaves,
+                                                     0) != hipSuccess ||
+        n < 1)
         n = 1;
     return n;
 }
@@ -1363,7 +1749,7 @@ int tiled_resident_per_cu()
 // Workgroups of the tiled kernel that are resident at once on the current
 // device (compute units x workgroups per compute unit); 256 when no device
 // can be queried.
-int tiled_resident(int bm, int wn)
+int tiled_resident(int bm, int wn, bool mfma32)
 {
     static std::mutex mu;
     static std::map<std::pair<int, int>, int> cache;  // (device, tile id) -> workgroups
@@ -1373,18 +1759,24 @@ int tiled_resident(int bm, int wn)
         (void)hipGetLastError();
         return 256;
     }
-    const int id = bm * 1000 + wn;
+    const int id = bm * 1000 + wn + (mfma32 ? 1000000 : 0);
     std::lock_guard<std::mutex> lk(mu);
     auto it = cache.find({dev, id});
     if (it != cache.end()) return it->second;
     int per = 1;
-    if (bm == 16 && wn == 16) per = tiled_resident_per_cu<16, 16>();
-    else if (bm == 16 && wn == 32) per = tiled_resident_per_cu<16, 32>();
-    else if (bm == 32 && wn == 16) per = tiled_resident_per_cu<32, 16>();
-    else if (bm == 32 && wn == 32) per = tiled_resident_per_cu<32, 32>();
-    else if (bm == 64 && wn == 32) per = tiled_resident_per_cu<64, 32>();
-    else if (bm == 64 && wn == 64) per = tiled_resident_per_cu<64, 64>();
-    else if (bm == 128 && wn == 32) per = tiled_resident_per_cu<128, 32>();
+    if (mfma32) {
+        if (bm == 32 && wn == 32) per = resident_per_cu(&tiled32_kernel<32, 32>);
+        else if (bm == 64 && wn == 32) per = resident_per_cu(&tiled32_kernel<64, 32>);
+        else if (bm == 128 && wn == 32) per = resident_per_cu(&tiled32_kernel<128, 32>);
+    } else if (bm == 16 && wn == 16) per = resident_per_cu(&tiled_kernel<16, 16>);
+    else if (bm == 16 && wn == 32) per = resident_per_cu(&tiled_kernel<16, 32>);
+    else if (bm == 32 && wn == 16) per = resident_per_cu(&tiled_kernel<32, 16>);
+    else if (bm == 32 && wn == 32) per = resident_per_cu(&tiled_kernel<32, 32>);
+    else if (bm == 64 && wn == 16) per = resident_per_cu(&tiled_kernel<64, 16>);
+    else if (bm == 64 && wn == 32) per = resident_per_cu(&tiled_kernel<64, 32>);
+    else if (bm == 128 && wn == 16) per = resident_per_cu(&tiled_kernel<128, 16>);
+    else if (bm == 64 && wn == 64) per = resident_per_cu(&tiled_kernel<64, 64>);
+    else if (bm == 128 && wn == 32) per = resident_per_cu(&tiled_kernel<128, 32>);
     (void)hipGetLastError();
     const int g = std::min(cus * per, kSkMaxWorkgroups);
     cache[{dev, id}] = g;
@@ -1448,14 +1840,34 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
         pl->bm = 32;
         pl->wn = 16;
     } else if (M <= 64) {
-        const bool wide = (int64_t)ceil_div(M, 64) * ceil_div(N, 256) >= 160;
+        // 64-row tiles of 16-column waves when they alone fill the chip,
+        // else 32-row ones (split below)
+        const bool wide = (int64_t)ceil_div(M, 64) * ceil_div(N, 128) >= 160;
         pl->bm = wide ? 64 : 32;
-        pl->wn = wide ? 32 : 16;
+        pl->wn = 16;
     } else {
-        // The largest tile whose K slices stay long: a split that leaves few
-        // k-groups per workgroup pays the pipeline fill and the partial-sum
-        // pass for little work, and a smaller tile that needs less splitting
-        // wins (narrow N or short K).
+        // Mid M with a short or medium K, when the 128 x 256 tiles are too
+        // few to fill the chip: 16-column waves on 128- or 64-row tiles
+        // (twice the workgroups of 32-column waves, each weight dequantized
+        // ceil(M / BM) times, and two workgroups per compute unit) when they
+        // fill it without splitting K.
+        bool mid = false;
+        if ((int64_t)ceil_div(M, 128) * ceil_div(N, 256) < 160 && KG < 128)
+            for (int bm : {128, 64})
+                if (!mid && (int64_t)ceil_div(M, bm) * ceil_div(N, 128) >= 160) {
+                    pl->bm = bm;
+                    pl->wn = 16;
+                    mid = true;
+                }
+        // Otherwise the largest tile whose K slices stay long: a split that
+        // leaves few k-groups per workgroup pays the pipeline fill and the
+        // partial-sum pass for little work, and a smaller tile that needs
+        // less splitting wins (narrow N or short K).
+        if (mid) {
+            pl->split = 1;
+            pl->kgps = 0;
+            return QUICK_OK;
+        }
         static const int cand[3][2] = {{128, 32}, {64, 32}, {32, 16}};
         for (int c = M <= 96 ? 1 : 0; c < 3; ++c) {
             pl->bm = cand[c][0];
@@ -1474,19 +1886,23 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
         return QUICK_OK;
     }
     pl->kgps = 0;
-    // At least half as many tiles as resident workgroups, but not a whole
-    // number of rounds, and a long K: stream-K spreads the tiles x k-groups
-    // work evenly and each split tile has only a few pieces to add.  Short K
-    // (each piece's pipeline fill and partial-tile traffic weigh more) or
-    // fewer tiles: split-K, whose separate reduction pass spreads the adding
-    // over the whole chip.
+    // More tiles than resident workgroups with the last round of tiles
+    // less than 70 % full, and a long K: stream-K spreads the tiles x
+    // k-groups work evenly and each split tile has only a few pieces to add.
+    // A fuller last round, or a single partial round, runs faster as whole
+    // tiles (the chip is power-limited under this load, so idle compute
+    // units cost less than the pieces' fix-ups).  Short K (each piece's
+    // pipeline fill and partial-tile traffic weigh more) or fewer tiles:
+    // split-K, whose separate reduction pass spreads the adding over the
+    // whole chip.
     const int64_t resident = tiled_resident(pl->bm, pl->wn);
-    if (pl->bm >= 64 && KG >= 48 && tiles % resident != 0 && 2 * tiles >= resident) {
+    const int64_t slots = (tiles + resident - 1) / resident * resident;
+    if (pl->bm >= 64 && KG >= 48 && tiles > resident && (slots - tiles) * 10 > 3 * slots) {
         pl->variant = kVariantStreamK;
         pl->split = 0;
         return QUICK_OK;
     }
-    const int64_t target = pl->wn == 16 ? (M > 64 ? 256 : 384) : 160;
+    const int64_t target = pl->wn == 16 ? (M > 64 ? 256 : M > 32 ? 160 : 384) : 160;
     int s = 1;
     while (tiles * s < target && KG / (2 * s) >= 4 && s < 8) s *= 2;
     pl->split = s;
@@ -1513,10 +1929,16 @@ bool tuned_config(int64_t M, int64_t N, int64_t K, quick_config_t* out)
     return true;
 }
 
+bool tiled32_supported(int bm, int wn)
+{
+    // (64 x 64 wave tiles spill registers in this form)
+    return (bm == 32 || bm == 64 || bm == 128) && wn == 32;
+}
+
 bool tiled_supported(int bm, int wn)
 {
-    return ((bm == 16 || bm == 32) && (wn == 16 || wn == 32)) || (bm == 64 && wn == 32) ||
-           (bm == 128 && wn == 32) || (bm == 64 && wn == 64);
+    return ((bm == 16 || bm == 32) && (wn == 16 || wn == 32)) || ((bm == 64 || bm == 128) && (wn == 16 || wn == 32)) ||
+           (bm == 64 && wn == 64);
 }
 
 int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* pl)
@@ -1526,7 +1948,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
     if (!cfg && tuned_config(M, N, K, &tuned)) cfg = &tuned;
     if (!cfg) return QUICK_OK;
     const int64_t KG = K / 128;
-    if (cfg->variant < 0 || cfg->variant > 5 || cfg->variant == 4 || cfg->split_k < 0) return QUICK_ERR_INVALID_ARG;
+    if (cfg->variant < 0 || cfg->variant > 7 || cfg->variant == 4 || cfg->split_k < 0) return QUICK_ERR_INVALID_ARG;
     if (cfg->variant == kVariantKStream) {
         // split_k: K slices (0 = auto; raised to the minimum); tile_n:
         // n-tiles per wave (0 = 2); the arrival counters cover every column
@@ -1553,16 +1975,21 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
             if (cfg->tile_n != 1 && cfg->tile_n != 2) return QUICK_ERR_INVALID_ARG;
             pl->wn = cfg->tile_n;
         }
-    } else if (cfg->variant == kVariantTiled || cfg->variant == kVariantStreamK) {
+    } else if (is_tiled(cfg->variant)) {
         if (!is_tiled(pl->variant)) {
             pl->bm = 64;
             pl->wn = 32;
             pl->split = 1;
         }
-        if (pl->variant != cfg->variant) pl->split = cfg->variant == kVariantStreamK ? 0 : 1;
+        if (is_streamk(pl->variant) != is_streamk(cfg->variant)) pl->split = is_streamk(cfg->variant) ? 0 : 1;
+        if (is_t32(cfg->variant)) {
+            // pairs of n-tiles, 32-row blocks
+            pl->wn = std::max(pl->wn, 32);
+            pl->bm = std::max(pl->bm, 32);
+        }
         pl->variant = cfg->variant;
     }
-    if (pl->variant == kVariantStreamK) {
+    if (is_streamk(pl->variant)) {
         // split_k: persistent workgroups, a multiple of 8 (0 = all resident)
         if (cfg->split_k && (cfg->split_k % 8 != 0 || cfg->split_k > kSkMaxWorkgroups))
             return QUICK_ERR_INVALID_ARG;
@@ -1578,11 +2005,12 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
             if (cfg->tile_n != 16 && cfg->tile_n != 32 && cfg->tile_n != 64) return QUICK_ERR_INVALID_ARG;
             pl->wn = cfg->tile_n;
         }
-        if (cfg->split_k && pl->variant == kVariantTiled) {
+        if (cfg->split_k && !is_streamk(pl->variant)) {
             if (cfg->split_k > KG) return QUICK_ERR_INVALID_ARG;
             pl->split = cfg->split_k;
         }
-        if (!tiled_supported(pl->bm, pl->wn)) return QUICK_ERR_INVALID_ARG;
+        if (is_t32(pl->variant) ? !tiled32_supported(pl->bm, pl->wn) : !tiled_supported(pl->bm, pl->wn))
+            return QUICK_ERR_INVALID_ARG;
     }
     return QUICK_OK;
 }
@@ -1600,21 +2028,22 @@ void finish_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
         pl->split = ceil_div(KG, pl->kgps);  // no empty slices
         return;
     }
-    if (pl->variant == kVariantStreamK) {
+    if (is_streamk(pl->variant)) {
         // 8 <= workgroups <= tiles x k-groups, a multiple of 8: every
         // workgroup gets a non-empty range and the XCD mapping is exact
         const int64_t units = (int64_t)ceil_div(M, pl->bm) * ceil_div(N, kTiledWaves * pl->wn) * (K / 128);
-        int64_t g = pl->split ? pl->split : tiled_resident(pl->bm, pl->wn);
+        int64_t g = pl->split ? pl->split : tiled_resident(pl->bm, pl->wn, is_t32(pl->variant));
         g = std::min<int64_t>(g, units) / 8 * 8;
         if (g >= 8) {
             pl->split = (int)g;
             pl->kgps = 0;
             return;
         }
-        pl->variant = kVariantTiled;  // too little work: one workgroup per tile
+        // too little work: one workgroup per tile
+        pl->variant = is_t32(pl->variant) ? kVariantTiled32 : kVariantTiled;
         pl->split = 1;
     }
-    if (pl->variant == kVariantTiled) {
+    if (pl->variant == kVariantTiled || pl->variant == kVariantTiled32) {
         const int64_t KG = K / 128;
         if (pl->split > KG) pl->split = (int)KG;
         if (pl->split < 1) pl->split = 1;
@@ -1629,9 +2058,9 @@ size_t plan_workspace(int64_t M, int64_t N, const Plan& pl)
 {
     if (pl.variant == kVariantKStream && pl.split > 1)
         return kSkCounterBytes + (size_t)ks_groups(N, pl.wn) * pl.split * kKsWaves * pl.wn * 1024;
-    if (pl.variant == kVariantTiled && pl.split > 1)
+    if ((pl.variant == kVariantTiled || pl.variant == kVariantTiled32) && pl.split > 1)
         return kSkCounterBytes + (size_t)pl.split * M * N * sizeof(float);
-    if (pl.variant == kVariantStreamK) return kSkCounterBytes + 2 * (size_t)pl.split * sk_slot_bytes(pl.bm, pl.wn);
+    if (is_streamk(pl.variant)) return kSkCounterBytes + 2 * (size_t)pl.split * sk_slot_bytes(pl.bm, pl.wn);
     return 0;
 }
 
@@ -1847,6 +2276,9 @@ int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16
         else if (pl.bm == 16 && pl.wn == 16) launch_tiled_t<16, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
         else if (pl.bm == 32 && pl.wn == 16) launch_tiled_t<32, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
         else if (pl.bm == 64 && pl.wn == 32) launch_tiled_t<64, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 64 && pl.wn == 16) launch_tiled_t<64, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
+        else if (pl.bm == 128 && pl.wn == 16)
+            launch_tiled_t<128, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
         else if (pl.bm == 128 && pl.wn == 32)
             launch_tiled_t<128, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
         else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
@@ -1857,6 +2289,46 @@ int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16
         const int64_t quads = rows * (epi.act ? N / 2 : N) / 4;
         hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, st,
                            ws + kSkCounterBytes / sizeof(float), y, rows, N, pl.split, epi);
+    }
+    return QUICK_OK;
+}
+
+template <int BM, int WN, bool EP>
+void launch_tiled32_e(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz,
+                      uint16_t* y, float* ws, int M, int N, int K, hipStream_t st, const Epi& epi)
+{
+    const int nm = ceil_div(M, BM);
+    const int nn = ceil_div(N, kTiledWaves * WN);
+    if (pl.variant == kVariantStreamK32) {
+        hipLaunchKernelGGL((tiled32_kernel<BM, WN, EP>), dim3(pl.split), dim3(64 * kTiledWaves), 0, st, x, pw, ps,
+                           pz, y, ws, M, N, K, 0, nm, nn, 0, epi);
+        return;
+    }
+    const int grid = ceil_div((int64_t)nm * nn * pl.split, 8) * 8;
+    hipLaunchKernelGGL((tiled32_kernel<BM, WN, EP>), dim3(grid), dim3(64 * kTiledWaves), 0, st, x, pw, ps, pz, y,
+                       ws, M, N, K, pl.kgps, nm, nn, pl.split, epi);
+}
+
+template <int BM, int WN>
+void launch_tiled32_t(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz,
+                      uint16_t* y, float* ws, int M, int N, int K, hipStream_t st, const Epi& epi)
+{
+    const bool split = pl.variant == kVariantTiled32 && pl.split > 1;
+    if ((epi.bias || epi.act) && !split) launch_tiled32_e<BM, WN, true>(pl, x, pw, ps, pz, y, ws, M, N, K, st, epi);
+    else launch_tiled32_e<BM, WN, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, epi);
+}
+
+int launch_tiled32(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16_t* ps, const uint32_t* pz,
+                   uint16_t* y, float* ws, int M, int N, int K, hipStream_t st, const Epi& epi)
+{
+    if (pl.bm == 32 && pl.wn == 32) launch_tiled32_t<32, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st, epi);
+    else if (pl.bm == 64 && pl.wn == 32) launch_tiled32_t<64, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st, epi);
+    else if (pl.bm == 128 && pl.wn == 32) launch_tiled32_t<128, 32>(pl, x, pw, ps, pz, y, ws, M, N, K, st, epi);
+    else return QUICK_ERR_INVALID_ARG;
+    if (pl.variant == kVariantTiled32 && pl.split > 1) {
+        const int64_t quads = (int64_t)M * (epi.act ? N / 2 : N) / 4;
+        hipLaunchKernelGGL(splitk_reduce_kernel, dim3((unsigned)((quads + 255) / 256)), dim3(256), 0, st,
+                           ws + kSkCounterBytes / sizeof(float), y, (int64_t)M, N, pl.split, epi);
     }
     return QUICK_OK;
 }
@@ -1889,6 +2361,7 @@ using quick::launch_ablation;
 using quick::launch_kstream;
 using quick::launch_stream;
 using quick::launch_tiled;
+using quick::launch_tiled32;
 
 bool grouped_tile_supported(int bm, int wn)
 {
@@ -1977,6 +2450,8 @@ int gemm_impl(const void* x, const void* packed, const void* scales, const void*
         st = launch_stream(pl, xx, pw, ps, pz, yy, (int)M, (int)N, (int)K, hs, epi);
     else if (pl.variant == kVariantKStream)
         st = launch_kstream(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs, epi);
+    else if (is_t32(pl.variant))
+        st = launch_tiled32(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs, epi);
     else
         st = launch_tiled(pl, xx, pw, ps, pz, yy, static_cast<float*>(ws), (int)M, (int)N, (int)K, hs, epi);
     if (st) return st;
@@ -2128,12 +2603,17 @@ std::vector<quick_config_t> tune_candidates(int64_t M, int64_t N, int64_t K)
     }
     int64_t mcap = 16;
     while (mcap < M && mcap < 128) mcap *= 2;
-    static const int tiles[][2] = {{16, 16}, {16, 32}, {32, 16}, {32, 32}, {64, 32}, {64, 64}, {128, 32}};
+    static const int tiles[][2] = {{16, 16}, {16, 32}, {32, 16}, {32, 32}, {64, 16}, {64, 32}, {64, 64},
+                                   {128, 16}, {128, 32}};
     for (const auto& t : tiles) {
         if (t[0] > mcap) continue;
         for (int s : {1, 2, 4, 8})
             if (s == 1 || KG / s >= 2) c.push_back(quick_config_t{kVariantTiled, s, t[0], t[1]});
         c.push_back(quick_config_t{kVariantStreamK, 0, t[0], t[1]});
+        if (!tiled32_supported(t[0], t[1])) continue;
+        for (int s : {1, 2, 4, 8})
+            if (s == 1 || KG / s >= 2) c.push_back(quick_config_t{kVariantTiled32, s, t[0], t[1]});
+        c.push_back(quick_config_t{kVariantStreamK32, 0, t[0], t[1]});
     }
     return c;
 }
@@ -2146,6 +2626,49 @@ std::vector<quick_config_t> tune_candidates(int64_t M, int64_t N, int64_t K)
 constexpr size_t kTuneSpan = (size_t)512 << 20;
 constexpr int kTuneMaxCopies = 64;
 
+namespace {
+
+// Time of `reps` launches of configuration c, each on the next weight copy,
+// as the best of kTrials replays of one HIP graph holding them (captured on
+// the private stream ts): the host's per-launch cost stays out of the timing
+// of kernels shorter than it.  QUICK_ERR_INVALID_ARG when c does not apply to
+// the shape.
+int tune_time(const void* x, const std::vector<const void*>& cw, const std::vector<const void*>& cs,
+              const std::vector<const void*>& cz, void* y, int64_t M, int64_t N, int64_t K, int64_t group,
+              hipStream_t ts, const quick_config_t& c, int reps, hipEvent_t e0, hipEvent_t e1, float* ms)
+{
+    constexpr int kTrials = 3;
+    const int ncopy = (int)cw.size();
+    // warm-up on ts: plans the launch and sizes ts's workspace outside the capture
+    int st = gemm_impl(x, cw[0], cs[0], cz[0], y, M, N, K, group, ts, &c, nullptr, 0);
+    if (st) return st;
+    hipGraph_t g = nullptr;
+    hipGraphExec_t ge = nullptr;
+    if (hipStreamBeginCapture(ts, hipStreamCaptureModeThreadLocal) != hipSuccess) return QUICK_ERR_HIP;
+    for (int r = 0; r < reps && !st; ++r) {
+        const int i = r % ncopy;
+        st = gemm_impl(x, cw[i], cs[i], cz[i], y, M, N, K, group, ts, &c, nullptr, 0);
+    }
+    const bool ended = hipStreamEndCapture(ts, &g) == hipSuccess;
+    if (!st && (!ended || hipGraphInstantiate(&ge, g, nullptr, nullptr, 0) != hipSuccess)) st = QUICK_ERR_HIP;
+    for (int t = 0; t <= kTrials && !st; ++t) {   // t == 0: a replay that is not timed
+        float tm = 0.f;
+        if (hipEventRecord(e0, ts) != hipSuccess || hipGraphLaunch(ge, ts) != hipSuccess ||
+            hipEventRecord(e1, ts) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+            hipEventElapsedTime(&tm, e0, e1) != hipSuccess) {
+            st = QUICK_ERR_HIP;
+            break;
+        }
+        if (t == 1 || (t > 1 && tm < *ms)) *ms = tm;
+    }
+    if (ge) (void)hipGraphExecDestroy(ge);
+    if (g) (void)hipGraphDestroy(g);
+    (void)hipGetLastError();
+    return st;
+}
+
+}  // namespace
+
 extern "C" int quick_tune(const void* x, const void* packed, const void* scales, const void* zeros, void* y,
                           int64_t M, int64_t N, int64_t K, int64_t group, void* stream, quick_config_t* best)
 {
@@ -2153,9 +2676,20 @@ extern "C" int quick_tune(const void* x, const void* packed, const void* scales,
     if (st) return st;
     if (M == 0) return QUICK_OK;
     hipStream_t hs = (hipStream_t)stream;
+    hipStreamCaptureStatus cs0 = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(hs, &cs0) != hipSuccess) return QUICK_ERR_HIP;
+    if (cs0 != hipStreamCaptureStatusNone) return QUICK_ERR_CAPTURE;
+    // the timings run on a private stream that first waits for the caller's
+    // (whose work may be producing the inputs)
+    hipStream_t ts = nullptr;
     hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+    if (hipStreamCreateWithFlags(&ts, hipStreamNonBlocking) != hipSuccess || hipEventCreate(&e0) != hipSuccess ||
+        hipEventCreate(&e1) != hipSuccess || hipEventRecord(e0, hs) != hipSuccess ||
+        hipStreamWaitEvent(ts, e0, 0) != hipSuccess) {
+        (void)hipGetLastError();
         if (e0) (void)hipEventDestroy(e0);
+        if (e1) (void)hipEventDestroy(e1);
+        if (ts) (void)hipStreamDestroy(ts);
         return QUICK_ERR_HIP;
     }
     // weight copies: copy 0 is the caller's; the others live in one
@@ -2179,41 +2713,22 @@ extern "C" int quick_tune(const void* x, const void* packed, const void* scales,
         cw[i] = b;
         cs[i] = b + al(wb);
         cz[i] = b + al(wb) + al(sb);
-        if (hipMemcpyAsync((void*)cw[i], packed, wb, hipMemcpyDeviceToDevice, hs) != hipSuccess ||
-            hipMemcpyAsync((void*)cs[i], scales, sb, hipMemcpyDeviceToDevice, hs) != hipSuccess ||
-            hipMemcpyAsync((void*)cz[i], zeros, zb, hipMemcpyDeviceToDevice, hs) != hipSuccess)
+        if (hipMemcpyAsync((void*)cw[i], packed, wb, hipMemcpyDeviceToDevice, ts) != hipSuccess ||
+            hipMemcpyAsync((void*)cs[i], scales, sb, hipMemcpyDeviceToDevice, ts) != hipSuccess ||
+            hipMemcpyAsync((void*)cz[i], zeros, zb, hipMemcpyDeviceToDevice, ts) != hipSuccess)
             st = QUICK_ERR_HIP;
     }
-    const int reps = std::max(10, ncopy);
-    constexpr int kTrials = 3;
+    const int reps = std::max(20, ncopy);
     float best_ms = 0.f;
     quick_config_t bestc{};
     bool found = false;
     for (const quick_config_t& c : tune_candidates(M, N, K)) {
         if (st) break;
-        st = gemm_impl(x, packed, scales, zeros, y, M, N, K, group, stream, &c, nullptr, 0);  // warm-up
+        float ms = 0.f;
+        st = tune_time(x, cw, cs, cz, y, M, N, K, group, ts, c, reps, e0, e1, &ms);
         if (st == QUICK_ERR_INVALID_ARG) {  // not supported for this shape
             st = QUICK_OK;
             continue;
-        }
-        if (st) break;
-        // the fastest of kTrials timings of `reps` launches: a single timing
-        // can catch a clock or memory hiccup and record a slow configuration
-        float ms = 0.f;
-        for (int t = 0; t < kTrials && !st; ++t) {
-            float tm = 0.f;
-            if (hipEventRecord(e0, hs) != hipSuccess) { st = QUICK_ERR_HIP; break; }
-            for (int r = 0; r < reps && !st; ++r) {
-                const int i = r % ncopy;
-                st = gemm_impl(x, cw[i], cs[i], cz[i], y, M, N, K, group, stream, &c, nullptr, 0);
-            }
-            if (st) break;
-            if (hipEventRecord(e1, hs) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
-                hipEventElapsedTime(&tm, e0, e1) != hipSuccess) {
-                st = QUICK_ERR_HIP;
-                break;
-            }
-            ms = t == 0 ? tm : std::min(ms, tm);
         }
         if (st) break;
         if (!found || ms < best_ms) {
@@ -2222,13 +2737,14 @@ extern "C" int quick_tune(const void* x, const void* packed, const void* scales,
             found = true;
         }
     }
+    // the copies and ts's launches are done before anything is freed or y
+    // is written on the caller's stream
+    if (hipStreamSynchronize(ts) != hipSuccess && !st) st = QUICK_ERR_HIP;
     (void)hipEventDestroy(e0);
     (void)hipEventDestroy(e1);
-    if (extra) {
-        // the copies may still be read by launches in flight
-        if (hipStreamSynchronize(hs) != hipSuccess && !st) st = QUICK_ERR_HIP;
-        (void)hipFree(extra);
-    }
+    (void)hipStreamDestroy(ts);
+    if (extra) (void)hipFree(extra);
+    (void)hipGetLastError();
     if (st) return st;
     if (!found) return QUICK_ERR_INVALID_ARG;
     {

@@ -63,8 +63,12 @@ int launch_kstream(const Plan& pl, const uint16_t* x, const lu4_t* pw, const uin
 int launch_tiled(const Plan& pl, const uint16_t* x, const lu4_t* pw, const uint16_t* ps, const uint32_t* pz,
                  uint16_t* y, float* ws, int M, int N, int K, hipStream_t st, const Epi& epi,
                  const GroupArgs* ga = nullptr);
-// Workgroups of the tiled kernel resident at once on the current device.
-int tiled_resident(int bm, int wn);
+// Workgroups of the tiled kernel (mfma32: its 32x32x16 form) resident at
+// once on the current device.
+int tiled_resident(int bm, int wn, bool mfma32 = false);
+// The tiled kernel on the 32x32x16 instruction (plans of variants 6 and 7).
+int launch_tiled32(const Plan& pl, const uint16_t* x, const lu4_t* pw, const uint16_t* ps, const uint32_t* pz,
+                   uint16_t* y, float* ws, int M, int N, int K, hipStream_t st, const Epi& epi);
 // The 64 x 256 data-parallel tiled kernel with the write-back mode of the
 // ablation (0 direct, 1 padded LDS rows, 2 unpadded LDS rows).
 int launch_ablation(const uint16_t* x, const lu4_t* pw, const uint16_t* ps, const uint32_t* pz, uint16_t* y,

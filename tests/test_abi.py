@@ -132,7 +132,17 @@ def test_gemm_ex_validation_without_device():
     L = Q.lib()
     def ex(cfg, M=4, N=4096, K=4096, ws=None, wsb=0):
         return L.quick_w4a16_gemm_ex(A, A, A, A, A, M, N, K, 128, None, ctypes.byref(cfg), ws, wsb)
-    assert ex(Q.make_config(variant=6)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=8)) == Q.QUICK_ERR_INVALID_ARG
+    # the 32x32x16 tiled form: 32-column waves over 32, 64 or 128 rows
+    assert ex(Q.make_config(variant=6, tile_m=64, tile_n=16)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=6, tile_m=64, tile_n=64)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=7, tile_m=16, tile_n=32)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=7, tile_m=128, split_k=12)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=6, split_k=33)) == Q.QUICK_ERR_INVALID_ARG
+    assert Q.workspace_bytes(256, 4096, 4096, Q.make_config(variant=6, tile_m=128, tile_n=32, split_k=4)) == \
+        Q.WS_COUNTER_BYTES + 4 * 256 * 4096 * 4
+    assert Q.workspace_bytes(256, 4096, 4096, Q.make_config(variant=7, tile_m=128, tile_n=32, split_k=64)) == \
+        Q.WS_COUNTER_BYTES + 2 * 64 * 128 * 256 * 4
     assert ex(Q.make_config(variant=5), M=17) == Q.QUICK_ERR_INVALID_ARG       # more than 16 rows
     assert ex(Q.make_config(variant=5, tile_n=3)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=5, tile_m=16)) == Q.QUICK_ERR_INVALID_ARG

@@ -20,11 +20,15 @@ from gpu_util import TOL, Packed, f16_values, from_dev_y, rand_case, rel_err, ru
 pytestmark = pytest.mark.gpu
 
 STREAM_CFGS = [dict(variant=1, split_k=w, tile_n=p) for w in (1, 2, 4, 8) for p in (1, 2)]
-TILES = ((16, 16), (16, 32), (32, 16), (32, 32), (64, 32), (64, 64), (128, 32))
+TILES = ((16, 16), (16, 32), (32, 16), (32, 32), (64, 16), (64, 32), (64, 64), (128, 16), (128, 32))
 TILED_CFGS = [dict(variant=2, tile_m=bm, tile_n=wn, split_k=s) for bm, wn in TILES for s in (1, 3)]
 # stream-K: 8 and 24 resident workgroups split most tiles across workgroups;
 # 0 = all resident workgroups (clamped to the work units)
 STREAMK_CFGS = [dict(variant=3, tile_m=bm, tile_n=wn, split_k=g) for bm, wn in TILES for g in (8, 24, 0)]
+# the tiled kernel on the 32x32x16 instruction (pairs of n-tiles, 32-row blocks)
+TILES32 = ((32, 32), (64, 32), (128, 32))
+TILED32_CFGS = ([dict(variant=6, tile_m=bm, tile_n=wn, split_k=s) for bm, wn in TILES32 for s in (1, 3)] +
+                [dict(variant=7, tile_m=bm, tile_n=wn, split_k=g) for bm, wn in TILES32 for g in (8, 24, 0)])
 
 
 def _check(M, K, N, cfg, seed):
@@ -62,6 +66,17 @@ def test_stream_ring_regimes(M, waves, npw):
 def test_tiled_variants(M, cfg):
     for K, N in ((384, 80), (640, 528)):
         _check(M, K, N, cfg, seed=M * 1000 + K + N + 7)
+
+
+@pytest.mark.parametrize("cfg", TILED32_CFGS,
+                         ids=lambda c: "v%d_bm%d_wn%d_s%d" % (c["variant"], c["tile_m"], c["tile_n"], c["split_k"]))
+@pytest.mark.parametrize("M", [1, 33, 65, 129, 300])
+def test_tiled32_variants(M, cfg):
+    """Ragged shapes: N not a multiple of the 32-column pair (a lone last
+    n-tile, clamped and never stored), M tails inside 32-row blocks, K slices
+    and stream-K pieces across tiles."""
+    for K, N in ((384, 80), (640, 528), (2304, 272)):
+        _check(M, K, N, cfg, seed=M * 1000 + K + N + 17)
 
 
 @pytest.mark.parametrize("cfg", STREAMK_CFGS, ids=lambda c: "bm%d_wn%d_g%d" % (c["tile_m"], c["tile_n"], c["split_k"]))
@@ -125,7 +140,10 @@ def test_c1_toy_full_output():
 
 @pytest.mark.parametrize("cfg", [None, dict(variant=1, split_k=4, tile_n=2), dict(variant=2, tile_m=64, tile_n=32, split_k=2),
                                  dict(variant=2, tile_m=128, tile_n=32, split_k=1),
-                                 dict(variant=5, split_k=3, tile_n=1), dict(variant=5, split_k=1, tile_n=2)])
+                                 dict(variant=5, split_k=3, tile_n=1), dict(variant=5, split_k=1, tile_n=2),
+                                 dict(variant=6, tile_m=128, tile_n=32, split_k=1),
+                                 dict(variant=6, tile_m=32, tile_n=32, split_k=2),
+                                 dict(variant=7, tile_m=64, tile_n=32, split_k=16)])
 def test_one_hot_rows_give_exact_dequant(cfg):
     """x row m = e_{k_m}: y[m][n] is a single product, so it must equal the
     binary16 rounding of (q - z) * s exactly."""
@@ -145,7 +163,8 @@ def test_one_hot_rows_give_exact_dequant(cfg):
 KSTREAM_EXACT = [dict(variant=5, split_k=1, tile_n=2), dict(variant=5, split_k=5, tile_n=1)]
 
 
-@pytest.mark.parametrize("cfg", [None] + STREAM_CFGS[::3] + TILED_CFGS[::3] + STREAMK_CFGS[::4] + KSTREAM_EXACT)
+@pytest.mark.parametrize("cfg", [None] + STREAM_CFGS[::3] + TILED_CFGS[::3] + STREAMK_CFGS[::4] + KSTREAM_EXACT +
+                         TILED32_CFGS[::2])
 def test_integer_data_exact_under_any_split(cfg):
     """s = 1, z = 8, q in {7,8,9}, x in {-1,0,1}: every partial sum is a small
     integer, so any summation order is exact and y equals int64 x . (q - z)."""

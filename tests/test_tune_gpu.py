@@ -32,3 +32,29 @@ def test_tune_records_fastest_and_auto_uses_it(M, K, N):
         assert rel_err(y_auto, ref) <= TOL
     finally:
         Q.tune_table_clear()
+
+
+def test_tune_refused_under_capture():
+    """quick_tune allocates and synchronizes: on a capturing stream it
+    returns QUICK_ERR_CAPTURE and records nothing."""
+    Q.tune_table_clear()
+    M, K, N = 16, 1024, 272
+    x, q, z, s = rand_case(801, M, K, N)
+    p = Packed(q, z, s)
+    xd = to_dev_x(x)
+    y = torch.empty((M, N), dtype=torch.float16, device="cuda")
+    marker = torch.zeros(4, device="cuda")
+    side = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    status = None
+    with torch.cuda.graph(g, stream=side):
+        marker.fill_(1.0)
+        try:
+            Q.tune(xd, p.dw, p.ds, p.dz, N, y=y)
+        except Q.QuickError as e:
+            status = e.status
+    assert status == Q.QUICK_ERR_CAPTURE
+    assert Q.tune_table_size() == 0
+    g.replay()
+    torch.cuda.synchronize()
+    assert bool((marker == 1.0).all())
