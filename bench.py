@@ -119,12 +119,36 @@ def whole_repetitions(names, seq):
     return reps
 
 
-def ingest_pmc(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, points, dominant):
-    """HBM bytes per launch of the dominant kernel from FETCH_SIZE / WRITE_SIZE
-    runs of one bench step, each scaled by what the counter reads for a plain
-    device-to-device copy of COPY_CAL_BYTES."""
+def launch_points(points):
+    """Index of the point each launch of launch_sequence(points) belongs to."""
+    idx = []
+    for i, p in enumerate(points):
+        idx.append(i)
+        if p["sel"]["variant"] in (2, 6) and p["sel"]["split_k"] > 1:
+            idx.append(i)   # its split-K reduction pass
+    return idx
+
+
+TRAFFIC_MD = os.path.join(ROOT, "profiles", "traffic_per_gemm_llama2_7b_70b.md")
+PMC_COMMANDS = "\n".join(
+    "timeout -s KILL 300 rocprofv3 --pmc %s --output-format csv -d <dir> -o %s -- python3 <repo>/bench.py %s" % (
+        c, o, a) for c, o, a in (("FETCH_SIZE", "f", "--steps 1 --warmup 0 --no-cpu-baseline"),
+                                ("WRITE_SIZE", "w", "--steps 1 --warmup 0 --no-cpu-baseline"),
+                                ("FETCH_SIZE", "cf", "--copy-calibration"),
+                                ("WRITE_SIZE", "cw", "--copy-calibration")))
+
+
+def ingest_pmc(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, points, dominant, out_md=TRAFFIC_MD,
+               command=""):
+    """HBM bytes from FETCH_SIZE / WRITE_SIZE runs of one bench step, each
+    scaled by what the counter reads for a plain device-to-device copy of
+    COPY_CAL_BYTES: per launch of the dominant kernel (returned, for the
+    stored roofline traffic) and per GEMM of the step (split-K reduction
+    included), written as a markdown table against the algorithmic bytes."""
     seq = launch_sequence(points)
+    lp = launch_points(points)
     per = {}
+    per_point = {}
     for name, path in (("FETCH_SIZE", fetch_csv), ("WRITE_SIZE", write_csv)):
         ours = [r for r in read_counter_csv(path, name)
                 if "anonymous namespace)::" in r[1] and "at::" not in r[1]]
@@ -139,6 +163,10 @@ def ingest_pmc(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, points, domin
         if not vals:
             raise SystemExit("no launch of %s in the step" % dominant)
         per[name] = float(np.mean(vals))
+        acc = np.zeros(len(points))
+        for k in range(reps * len(seq)):
+            acc[lp[k % len(seq)]] += ours[k][2]
+        per_point[name] = acc / reps
     cal = {}
     for name, path in (("FETCH_SIZE", cal_fetch_csv), ("WRITE_SIZE", cal_write_csv)):
         # the device-to-device copies of the calibration run (HIP runtime copy kernel)
@@ -147,6 +175,29 @@ def ingest_pmc(fetch_csv, write_csv, cal_fetch_csv, cal_write_csv, points, domin
         cal[name] = (COPY_CAL_BYTES / 1024.0) / float(np.median([x for x in v if x >= 0.9 * top]))
     fetch_b = per["FETCH_SIZE"] * cal["FETCH_SIZE"] * 1024.0
     write_b = per["WRITE_SIZE"] * cal["WRITE_SIZE"] * 1024.0
+    if out_md:
+        lines = ["| cfg | shape | K | N | M | kernel | fetched MB | written MB | alg. read MB | alg. write MB | "
+                 "fetched / alg. read | written / alg. write |", "|---|---|---|---|---|---|---|---|---|---|---|---|"]
+        for i, p in enumerate(points):
+            fb = per_point["FETCH_SIZE"][i] * cal["FETCH_SIZE"] * 1024.0
+            wb = per_point["WRITE_SIZE"][i] * cal["WRITE_SIZE"] * 1024.0
+            aw = 2 * p["M"] * p["N"]
+            ar = p["bytes"] - aw
+            lines.append("| C%d | %s | %d | %d | %d | %s | %.2f | %.2f | %.2f | %.2f | %.2f | %.2f |" % (
+                p["cid"], p["shape"], p["K"], p["N"], p["M"], p["kernel"], fb / 1e6, wb / 1e6, ar / 1e6, aw / 1e6,
+                fb / ar, wb / aw))
+        with open(out_md, "w") as f:
+            f.write("# HBM traffic per GEMM of the bench step (rocprofv3 FETCH_SIZE / WRITE_SIZE)\n\n")
+            f.write("Commands (from the repository root on an MI355X, after `cd /tmp && export TMPDIR=/tmp`), "
+                    "each counter in a run of its own:\n\n```\n%s\n```\n\n" % command)
+            f.write("Then `python bench.py --ingest-pmc <fetch.csv> <write.csv> <cal_fetch.csv> <cal_write.csv>` "
+                    "(CPU).  Means over %d repetitions of the step's launch sequence; a split GEMM includes its "
+                    "reduction pass.  Counter readings are scaled by a plain %d MiB device-to-device copy of the same "
+                    "run type: FETCH_SIZE x %.3f, WRITE_SIZE x %.3f.  Algorithmic read bytes = packed weights, scales, "
+                    "zeros and x (each once); algorithmic write bytes = y.  FETCH_SIZE counts L2 misses, which "
+                    "include reads served by the Infinity Cache.\n\n" % (
+                        reps, COPY_CAL_BYTES >> 20, cal["FETCH_SIZE"], cal["WRITE_SIZE"]))
+            f.write("\n".join(lines) + "\n")
     return {
         "kernel": dominant,
         "kernel_source_sha256_16": kernel_source_digest(),
@@ -265,16 +316,29 @@ def ingest_mfma(csv_path, points, out_md, command):
     run of MFMA_COUNTERS over this script (--steps 1 --warmup 0): busy cycles
     of the matrix units over the GPU's active cycles times the SIMDs (the
     profiler's MfmaUtil), the matrix operations issued against the GEMM's
-    algorithmic flops, and the LDS instruction and bank-conflict counts."""
+    algorithmic flops, the vector-ALU instructions against those of one
+    dequantization of every weight, the LDS instruction and bank-conflict
+    counts, and the achieved clock of the longer launches."""
     import csv
     seq = launch_sequence(points)
     disp = {}
+    copies = []   # (duration ns, GRBM_GUI_ACTIVE) of the runtime's copy kernels
     for r in csv.DictReader(open(csv_path)):
         name = r["Kernel_Name"]
+        dur = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        if "copyBuffer" in name and r["Counter_Name"] == "GRBM_GUI_ACTIVE":
+            copies.append((dur, float(r["Counter_Value"])))
         if "anonymous namespace)::" not in name or "at::" in name:
             continue
-        d = disp.setdefault(int(r["Dispatch_Id"]), {"name": name})
+        d = disp.setdefault(int(r["Dispatch_Id"]), {"name": name, "dur": dur})
         d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    # GRBM_GUI_ACTIVE covers a window a fixed number of cycles longer than the
+    # dispatch: fit cycles per XCD = clock x duration + window over the copy
+    # kernels of the run (lightly loaded, so one clock) and take the window out
+    window = 0.0
+    if len(copies) >= 3:
+        cd = np.array(copies, dtype=np.float64)
+        _, window = np.polyfit(cd[:, 0], cd[:, 1] / MI355X_XCDS, 1)
     ids = sorted(disp)
     names = [disp[i]["name"] for i in ids]
     reps = whole_repetitions(names, seq)
@@ -285,28 +349,42 @@ def ingest_mfma(csv_path, points, out_md, command):
     for _ in range(reps):
         for i, p in enumerate(points):
             d = disp[ids[j]]   # the GEMM kernel itself (a split-K reduction follows it)
-            for c in MFMA_COUNTERS:
+            for c in MFMA_COUNTERS + ("dur",):
                 acc[i].setdefault(c, []).append(d.get(c, 0.0))
             j += 2 if (p["sel"]["variant"] in (2, 6) and p["sel"]["split_k"] > 1) else 1
-    lines = ["| cfg | shape | K | N | M | kernel | matrix busy % | matrix flops / algorithmic | LDS instr | LDS bank conflicts |",
-             "|---|---|---|---|---|---|---|---|---|---|"]
+    lines = ["| cfg | shape | K | N | M | kernel | matrix busy % | matrix flops / algorithmic | VALU / one dequant | "
+             "clock GHz | LDS instr | LDS bank conflicts |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|"]
     for i, p in enumerate(points):
         a = {c: float(np.mean(v)) for c, v in acc[i].items()}
         active = a["GRBM_GUI_ACTIVE"] / MI355X_XCDS
         util = 100.0 * a["SQ_VALU_MFMA_BUSY_CYCLES"] / (active * MI355X_SIMDS) if active else 0.0
         mflops = a["SQ_INSTS_VALU_MFMA_MOPS_F16"] * 512
-        lines.append("| C%d | %s | %d | %d | %d | %s | %.1f | %.2f | %.3g | %.3g |" % (
+        # one dequantization of every weight: 13 wave instructions per 64 lanes x 8 weights
+        deq = 13.0 * p["K"] * p["N"] / 512.0
+        clock = (active - window) / a["dur"] if a["dur"] >= 20000 else float("nan")
+        lines.append("| C%d | %s | %d | %d | %d | %s | %.1f | %.2f | %.2f | %s | %.3g | %.3g |" % (
             p["cid"], p["shape"], p["K"], p["N"], p["M"], p["kernel"], util, mflops / p["flops"],
-            a["SQ_INSTS_LDS"], a["SQ_LDS_BANK_CONFLICT"]))
+            a["SQ_INSTS_VALU"] / deq, "%.2f" % clock if clock == clock else "-", a["SQ_INSTS_LDS"],
+            a["SQ_LDS_BANK_CONFLICT"]))
     with open(out_md, "w") as f:
         f.write("# Matrix-core utilisation per GEMM of the bench step (rocprofv3 counters)\n\n")
         f.write("Command (from the repository root on an MI355X, after `cd /tmp && export TMPDIR=/tmp`):\n\n")
         f.write("```\n%s\n```\n\n" % command)
         f.write("Then `python bench.py --ingest-mfma <counter_collection.csv>` (CPU). %d repetitions of the step's "
                 "launch sequence; values are means per GEMM kernel launch (the split-K reduction pass is not "
-                "included). matrix busy %% = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / %d XCDs x %d SIMDs), "
-                "the profiler's MfmaUtil; matrix flops = SQ_INSTS_VALU_MFMA_MOPS_F16 x 512 against 2MNK "
-                "(above 1 where M is padded to 16-row blocks).\n\n" % (reps, MI355X_XCDS, MI355X_SIMDS))
+                "included).\n\n"
+                "* matrix busy %% = SQ_VALU_MFMA_BUSY_CYCLES / (GRBM_GUI_ACTIVE / %d XCDs x %d SIMDs), the "
+                "profiler's MfmaUtil.\n"
+                "* matrix flops = SQ_INSTS_VALU_MFMA_MOPS_F16 x 512 against 2MNK (above 1 where M is padded to "
+                "16-row blocks).\n"
+                "* VALU / one dequant = SQ_INSTS_VALU (all vector-ALU wave instructions of the launch, address "
+                "arithmetic and epilogue included) over 13 K N / 512, the instructions of dequantizing every weight "
+                "once (13 per 8 weights of 64 lanes); a tiled launch dequantizes each weight once per row tile.\n"
+                "* clock = (GRBM_GUI_ACTIVE / %d XCDs - window) / kernel duration (counter-run timestamps), for "
+                "launches of at least 20 us; window = %.0f cycles, the fixed excess of the counter window over the "
+                "dispatch, fitted over the run's runtime copy kernels.\n\n" % (
+                    reps, MI355X_XCDS, MI355X_SIMDS, MI355X_XCDS, window))
         f.write("\n".join(lines) + "\n")
     return reps
 
@@ -745,7 +823,7 @@ def main():
             p["sel"] = Q.select_config(p["M"], p["N"], p["K"])
             p["kernel"] = kernel_name(p["sel"])
             p["bytes"] = W.alg_bytes(p["M"], p["N"], p["K"])
-        t = ingest_pmc(*args.ingest_pmc, points, args.dominant)
+        t = ingest_pmc(*args.ingest_pmc, points, args.dominant, command=PMC_COMMANDS)
         os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
         with open(TRAFFIC_FILE, "w") as f:
             json.dump(t, f, indent=1)

@@ -1703,7 +1703,11 @@ splitk_reduce_kernel(const float* __restrict__ ws, uint16_t* __restrict__ y, int
 // Host side: validation, configuration, workspace, launch.
 // ---------------------------------------------------------------------------
 constexpr int kVariantStream = 1;
-[[maybe_unused]] constexpr size_t kStreamLdsX = 64 * 1024;  // LDS bytes the stream kernel may give to activations
+// LDS bytes the stream kernel may give to activations: gfx950's 160 KiB
+// less the 16 KiB its waves' partial sums take at most (a workgroup above
+// 80 KiB then has its compute unit to itself)
+[[maybe_unused]] constexpr size_t kStreamLdsX = 144 * 1024;
+[[maybe_unused]] constexpr size_t kDefaultLds = 64 * 1024;   // dynamic LDS without a raised limit
 constexpr int kVariantTiled = 2;
 constexpr int kVariantStreamK = 3;  // tiled kernel, stream-K schedule
 // (variant 4, a balanced stream kernel, was withdrawn: it never won on a
@@ -2146,10 +2150,12 @@ void launch_stream_t(const uint16_t* x, const u4_t* pw, const uint16_t* ps, cons
     const size_t xbytes = (size_t)WAVES * stream_slice_bytes(M, K / 128, WAVES);
     // (only single-block tiles stage x: no staged instantiation for MT > 1)
     if constexpr (MT == 1) {
-        if (xbytes <= kStreamLdsX) {
-            constexpr int D = NPW == 1 ? 8 : 4;
-            hipLaunchKernelGGL((stream_kernel<MT, NPW, WAVES, D, true>), grid, dim3(64 * WAVES), xbytes, st,
-                               x, pw, ps, pz, y, M, N, K, epi);
+        constexpr int D = NPW == 1 ? 8 : 4;
+        auto* kern = &stream_kernel<MT, NPW, WAVES, D, true>;
+        // more than the default dynamic LDS needs the kernel's limit raised
+        if (xbytes <= kDefaultLds ||
+            (xbytes <= kStreamLdsX && lds_limit_set(reinterpret_cast<const void*>(kern), kStreamLdsX))) {
+            hipLaunchKernelGGL(kern, grid, dim3(64 * WAVES), xbytes, st, x, pw, ps, pz, y, M, N, K, epi);
             return;
         }
     }
