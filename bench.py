@@ -362,10 +362,13 @@ def ingest_mfma(csv_path, points, out_md, command):
         mflops = a["SQ_INSTS_VALU_MFMA_MOPS_F16"] * 512
         # one dequantization of every weight: 13 wave instructions per 64 lanes x 8 weights
         deq = 13.0 * p["K"] * p["N"] / 512.0
+        # SQ_INSTS_VALU counts the matrix instructions too (16384 flops each,
+        # 32768 for the 32x32x16 form)
+        mfma_insts = mflops / (32768.0 if p["kernel"].startswith("tiled32") else 16384.0)
         clock = (active - window) / a["dur"] if a["dur"] >= 20000 else float("nan")
         lines.append("| C%d | %s | %d | %d | %d | %s | %.1f | %.2f | %.2f | %s | %.3g | %.3g |" % (
             p["cid"], p["shape"], p["K"], p["N"], p["M"], p["kernel"], util, mflops / p["flops"],
-            a["SQ_INSTS_VALU"] / deq, "%.2f" % clock if clock == clock else "-", a["SQ_INSTS_LDS"],
+            (a["SQ_INSTS_VALU"] - mfma_insts) / deq, "%.2f" % clock if clock == clock else "-", a["SQ_INSTS_LDS"],
             a["SQ_LDS_BANK_CONFLICT"]))
     with open(out_md, "w") as f:
         f.write("# Matrix-core utilisation per GEMM of the bench step (rocprofv3 counters)\n\n")
@@ -378,9 +381,11 @@ def ingest_mfma(csv_path, points, out_md, command):
                 "profiler's MfmaUtil.\n"
                 "* matrix flops = SQ_INSTS_VALU_MFMA_MOPS_F16 x 512 against 2MNK (above 1 where M is padded to "
                 "16-row blocks).\n"
-                "* VALU / one dequant = SQ_INSTS_VALU (all vector-ALU wave instructions of the launch, address "
+                "* VALU / one dequant = the launch's vector-ALU wave instructions other than matrix instructions "
+                "(SQ_INSTS_VALU, which counts those too, less the matrix instructions from the MOPS count; address "
                 "arithmetic and epilogue included) over 13 K N / 512, the instructions of dequantizing every weight "
-                "once (13 per 8 weights of 64 lanes); a tiled launch dequantizes each weight once per row tile.\n"
+                "once (13 per 8 weights of 64 lanes); a tiled launch dequantizes each weight once per row tile, so "
+                "the ideal is the number of row tiles, ceil(M / BM).\n"
                 "* clock = (GRBM_GUI_ACTIVE / %d XCDs - window) / kernel duration (counter-run timestamps), for "
                 "launches of at least 20 us; window = %.0f cycles, the fixed excess of the counter window over the "
                 "dispatch, fitted over the run's runtime copy kernels.\n\n" % (
