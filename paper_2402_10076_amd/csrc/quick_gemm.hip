@@ -593,9 +593,10 @@ stream_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
 //  * split-K (n_splits > 1): one workgroup per (tile, K slice); each writes
 //    fp32 partial sums to the workspace and a second kernel adds them in
 //    split order;
-//  * stream-K (n_splits == 0): gridDim.x resident workgroups share the
-//    tiles x k-groups iteration space in equal contiguous ranges, so no
-//    round of tiles runs on a partly idle chip.  A tile whose k-groups span
+//  * stream-K (n_splits == 0): gridDim.x resident workgroups run the whole
+//    rounds of tiles data-parallel and share the rest of the tiles x
+//    k-groups iteration space in equal contiguous ranges, so no round of
+//    tiles runs on a partly idle chip.  A tile whose k-groups span
 //    several workgroups is finished by the last of them to arrive (per-tile
 //    arrival counter): every contributor writes its fp32 partial tile with
 //    device-coherent stores, and the last one adds all partials in k order
@@ -1010,13 +1011,19 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         return;
     }
 
-    // ---- stream-K: this workgroup owns units [u0, u1) of tiles x k-groups
-    // (the host launches 8 <= gridDim.x <= tiles * KG, a multiple of 8, so
-    // every range is non-empty and a tile's contributors are consecutive)
-    const int64_t U = (int64_t)n_mt * n_ntiles * KG;
+    // ---- stream-K: whole rounds of tiles first, one tile per workgroup
+    // (tiles wid, wid + G, ..), then the remaining tiles x k-groups units in
+    // equal contiguous ranges: this workgroup owns units [u0, u1) of them.
+    // The host launches 8 <= gridDim.x <= tiles * KG, a multiple of 8; the
+    // stream-K part keeps at least gridDim.x units, so every range is
+    // non-empty and a tile's contributors are consecutive.  Workgroups of
+    // one XCD take consecutive ranges, so at any moment they work on a few
+    // n-tiles at the same k offset (shared in L2); a stream-K partition of
+    // every tile would start them at staggered k offsets instead.
+    int64_t U = (int64_t)n_mt * n_ntiles * KG;
     int G = gridDim.x;
     int wid = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
-    int64_t u0, u1;
+    int64_t u0, u1, ub = 0;
     if constexpr (GRP) {
         // the unit count is known only here: use the largest multiple of 8
         // workgroups not above it (the rest exit), or, with fewer than 8
@@ -1026,16 +1033,30 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
             if ((int)(blockIdx.x >> 3) >= (ge >> 3)) return;
             G = ge;
             wid = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
-            u0 = (int64_t)wid * U / G;
-            u1 = (int64_t)(wid + 1) * U / G;
         } else {
             if ((int64_t)blockIdx.x * KG >= U) return;
-            u0 = (int64_t)blockIdx.x * KG;
-            u1 = u0 + KG;
+            G = 0;
         }
+    }
+    if (G == 0) {
+        u0 = (int64_t)blockIdx.x * KG;
+        u1 = u0 + KG;
     } else {
-        u0 = (int64_t)wid * U / G;
-        u1 = (int64_t)(wid + 1) * U / G;
+        const int T = n_mt * n_ntiles;
+        int tdp = T / G * G;
+        // the stream-K part takes 1/2 to 3/2 tiles per workgroup: smaller
+        // pieces cost more in fix-ups than the idle compute units they save
+        if (tdp > 0 && tdp < T && (2 * (T - tdp) < G || (int64_t)(T - tdp) * KG < G)) tdp -= G;
+        for (int t = wid; t < tdp; t += G) {
+            set_tile(t);
+            run(0, KG);
+            store_y(acc);
+            __syncthreads();  // LDS stages are reused by the next tile
+        }
+        ub = (int64_t)tdp * KG;
+        U -= ub;
+        u0 = ub + (int64_t)wid * U / G;
+        u1 = ub + (int64_t)(wid + 1) * U / G;
     }
     unsigned* counters = reinterpret_cast<unsigned*>(ws);
     // partial-tile slot: thread-major f4 at ((wave * NP + p) * MTT + mt) * 64 + lane
@@ -1054,7 +1075,7 @@ tiled_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         if (kb == 0 && ke == KG) {
             store_y(acc);
         } else {
-            const int64_t tb = (int64_t)tt * KG;
+            const int64_t tb = (int64_t)tt * KG - ub;            // stream-K units before the tile
             const int w0 = (int)(((tb + 1) * G - 1) / U);        // owner of the tile's first unit
             const int w1 = (int)(((tb + KG) * G - 1) / U);       // ... and of its last
             // slot 2w: the piece that starts w's range; 2w+1: the piece that ends it
@@ -1595,13 +1616,24 @@ tiled32_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         return;
     }
 
-    // ---- stream-K (see tiled_kernel): equal contiguous ranges of the
-    // tiles x k-groups units, last-arriver fix-up in k order
-    const int64_t U = (int64_t)n_mtiles * n_ntiles * KG;
+    // ---- stream-K (see tiled_kernel): whole rounds of tiles first, then
+    // equal contiguous ranges of the remaining tiles x k-groups units,
+    // last-arriver fix-up in k order
+    const int T = n_mtiles * n_ntiles;
     const int G = gridDim.x;
     const int wid = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
-    const int64_t u0 = (int64_t)wid * U / G;
-    const int64_t u1 = (int64_t)(wid + 1) * U / G;
+    int tdp = T / G * G;
+    if (tdp > 0 && tdp < T && (2 * (T - tdp) < G || (int64_t)(T - tdp) * KG < G)) tdp -= G;
+    for (int t = wid; t < tdp; t += G) {
+        set_tile(t);
+        run(0, KG);
+        store_y(acc);
+        __syncthreads();  // LDS stages are reused by the next tile
+    }
+    const int64_t ub = (int64_t)tdp * KG;
+    const int64_t U = (int64_t)T * KG - ub;
+    const int64_t u0 = ub + (int64_t)wid * U / G;
+    const int64_t u1 = ub + (int64_t)(wid + 1) * U / G;
     unsigned* counters = reinterpret_cast<unsigned*>(ws);
     // partial-tile slot: thread-major f4 at (((wave * NPR + pr) * MB + mb) * 4 + b) * 64 + lane
     constexpr uint32_t SLOT_BYTES = (uint32_t)WAVES * NPR * MB * 4 * 64 * 16;
@@ -1619,7 +1651,7 @@ tiled32_kernel(const uint16_t* __restrict__ x, const u4_t* __restrict__ pw,
         if (kb == 0 && ke == KG) {
             store_y(acc);
         } else {
-            const int64_t tb = (int64_t)tt * KG;
+            const int64_t tb = (int64_t)tt * KG - ub;
             const int w0 = (int)(((tb + 1) * G - 1) / U);
             const int w1 = (int)(((tb + KG) * G - 1) / U);
             const uint32_t mine = uniform((uint32_t)(2 * wid + (u == u0 ? 0 : 1)) * SLOT_BYTES);
@@ -1891,17 +1923,17 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
     }
     pl->kgps = 0;
     // More tiles than resident workgroups with the last round of tiles
-    // less than 70 % full, and a long K: stream-K spreads the tiles x
-    // k-groups work evenly and each split tile has only a few pieces to add.
-    // A fuller last round, or a single partial round, runs faster as whole
-    // tiles (the chip is power-limited under this load, so idle compute
-    // units cost less than the pieces' fix-ups).  Short K (each piece's
-    // pipeline fill and partial-tile traffic weigh more) or fewer tiles:
-    // split-K, whose separate reduction pass spreads the adding over the
-    // whole chip.
+    // less than 75 % full, and a long K: stream-K runs the whole rounds as
+    // tiles and spreads the rest of the tiles x k-groups work evenly, each
+    // split tile having only a few pieces to add.  A nearly full last round,
+    // or a single partial round, runs faster as whole tiles (the chip is
+    // power-limited under this load, so idle compute units cost less than
+    // the pieces' fix-ups).  Short K (each piece's pipeline fill and
+    // partial-tile traffic weigh more) or fewer tiles: split-K, whose
+    // separate reduction pass spreads the adding over the whole chip.
     const int64_t resident = tiled_resident(pl->bm, pl->wn);
     const int64_t slots = (tiles + resident - 1) / resident * resident;
-    if (pl->bm >= 64 && KG >= 48 && tiles > resident && (slots - tiles) * 10 > 3 * slots) {
+    if (pl->bm >= 64 && KG >= 48 && tiles > resident && (slots - tiles) * 4 > slots) {
         pl->variant = kVariantStreamK;
         pl->split = 0;
         return QUICK_OK;

@@ -113,6 +113,20 @@ def test_streamk_many_pieces_per_tile(G):
     _check(100, 4096, 256, dict(variant=3, tile_m=128, tile_n=32, split_k=G), seed=G + 1)
 
 
+@pytest.mark.parametrize("rounds", [1.0, 2.0, 2.25, 2.5, 3.75])
+@pytest.mark.parametrize("variant,wn", [(3, 16), (7, 32)])
+def test_streamk_rounds_then_pieces(rounds, variant, wn):
+    """Stream-K on 16 workgroups runs whole rounds of tiles one per workgroup,
+    then splits the rest of the tiles: whole rounds only (1, 2), a quarter
+    round merged into the last whole one (2.25), a half and three quarters
+    of a round in pieces (2.5, 3.75)."""
+    G, bm = 16, 32
+    T = int(rounds * G)
+    M = 4 * bm                      # 4 m-tiles per n-tile
+    N = (T // 4) * 8 * wn           # T / 4 n-tiles of 8 waves x wn columns
+    _check(M, 1024, N, dict(variant=variant, tile_m=bm, tile_n=wn, split_k=G), seed=int(rounds * 100) + variant)
+
+
 @pytest.mark.parametrize("M", [1, 2, 5, 16, 31, 64, 65, 96, 127, 200, 513])
 def test_auto_config_small_shapes(M):
     _check(M, 1024, 272, None, seed=M)
