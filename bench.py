@@ -764,6 +764,10 @@ def main():
     ap.add_argument("--compare-fp16", action="store_true",
                     help="only compare the W4A16 GEMM with an fp16 GEMM through torch (hipBLASLt) on the "
                          "8192x8192 Llama-2-70B o_proj shape over M (context, not the metric)")
+    ap.add_argument("--compare-shape", default="8192,8192", metavar="K,N",
+                    help="with --compare-fp16: the weight shape")
+    ap.add_argument("--compare-m", default="1,4,16,32,64,128,256,512,1024,2048",
+                    help="with --compare-fp16: the batch sizes")
     ap.add_argument("--tune", action="store_true",
                     help="autotune every GEMM shape of the step during setup (untimed) before timing")
     ap.add_argument("--tune-save", default="", help="with --tune: write the tune table here")
@@ -868,8 +872,9 @@ def main():
                           "rows": read_ceiling()}))
         return
     if args.compare_fp16:
-        rows = compare_fp16(8192, 8192, [1, 4, 16, 32, 64, 128, 256, 512, 1024, 2048])
-        print(json.dumps({"compare": "w4a16 vs fp16 hipBLASLt", "K": 8192, "N": 8192, "rows": rows}))
+        ck, cn = (int(v) for v in args.compare_shape.split(","))
+        rows = compare_fp16(ck, cn, [int(m) for m in args.compare_m.split(",") if m])
+        print(json.dumps({"compare": "w4a16 vs fp16 hipBLASLt", "K": ck, "N": cn, "rows": rows}))
         return
     Q.lib()  # raises if the HIP library is not built
 
