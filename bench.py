@@ -311,18 +311,15 @@ MI355X_XCDS = 8
 MI355X_SIMDS = 256 * 4
 
 
-def ingest_mfma(csv_path, points, out_md, command):
-    """Matrix-core utilisation per GEMM of the step from one rocprofv3 --pmc
-    run of MFMA_COUNTERS over this script (--steps 1 --warmup 0): busy cycles
-    of the matrix units over the GPU's active cycles times the SIMDs (the
-    profiler's MfmaUtil), the matrix operations issued against the GEMM's
-    algorithmic flops, the vector-ALU instructions against those of one
-    dequantization of every weight, the LDS instruction and bank-conflict
-    counts, and the achieved clock of the longer launches."""
+def gemm_counters(csv_path, points, counters):
+    """Counter values of each GEMM kernel launch of the step from a rocprofv3
+    --pmc CSV: (whole repetitions of the launch sequence, per point a dict
+    counter -> list over repetitions (plus "dur", ns), and (duration ns,
+    GRBM_GUI_ACTIVE) of the runtime's copy kernels)."""
     import csv
     seq = launch_sequence(points)
     disp = {}
-    copies = []   # (duration ns, GRBM_GUI_ACTIVE) of the runtime's copy kernels
+    copies = []
     for r in csv.DictReader(open(csv_path)):
         name = r["Kernel_Name"]
         dur = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
@@ -332,13 +329,6 @@ def ingest_mfma(csv_path, points, out_md, command):
             continue
         d = disp.setdefault(int(r["Dispatch_Id"]), {"name": name, "dur": dur})
         d[r["Counter_Name"]] = d.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
-    # GRBM_GUI_ACTIVE covers a window a fixed number of cycles longer than the
-    # dispatch: fit cycles per XCD = clock x duration + window over the copy
-    # kernels of the run (lightly loaded, so one clock) and take the window out
-    window = 0.0
-    if len(copies) >= 3:
-        cd = np.array(copies, dtype=np.float64)
-        _, window = np.polyfit(cd[:, 0], cd[:, 1] / MI355X_XCDS, 1)
     ids = sorted(disp)
     names = [disp[i]["name"] for i in ids]
     reps = whole_repetitions(names, seq)
@@ -349,9 +339,65 @@ def ingest_mfma(csv_path, points, out_md, command):
     for _ in range(reps):
         for i, p in enumerate(points):
             d = disp[ids[j]]   # the GEMM kernel itself (a split-K reduction follows it)
-            for c in MFMA_COUNTERS + ("dur",):
+            for c in tuple(counters) + ("dur",):
                 acc[i].setdefault(c, []).append(d.get(c, 0.0))
             j += 2 if (p["sel"]["variant"] in (2, 6) and p["sel"]["split_k"] > 1) else 1
+    return reps, acc, copies
+
+
+WAIT_COUNTERS = ("SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_WAIT_INST_ANY", "SQ_ACTIVE_INST_ANY", "SQ_ACTIVE_INST_VALU",
+                 "SQ_ACTIVE_INST_LDS", "SQ_ACTIVE_INST_VMEM")
+WAITS_MD = os.path.join(ROOT, "profiles", "wave_states_bench_llama2_7b_70b.md")
+
+
+def ingest_waits(csv_path, points, out_md, command):
+    """Where the waves of each GEMM launch spend their time, from one
+    rocprofv3 --pmc run of WAIT_COUNTERS: each counter over SQ_WAVE_CYCLES
+    (all accumulate per wave, in the same units)."""
+    reps, acc, _ = gemm_counters(csv_path, points, WAIT_COUNTERS)
+    lines = ["| cfg | shape | K | N | M | kernel | us | waiting on a dependency | ready, not issued | issuing | "
+             "VALU | LDS | VMEM |", "|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for i, p in enumerate(points):
+        a = {c: float(np.mean(v)) for c, v in acc[i].items()}
+        wc = a["SQ_WAVE_CYCLES"] or 1.0
+        lines.append("| C%d | %s | %d | %d | %d | %s | %.1f | %.2f | %.2f | %.2f | %.2f | %.2f | %.2f |" % (
+            p["cid"], p["shape"], p["K"], p["N"], p["M"], p["kernel"], a["dur"] / 1000.0,
+            a["SQ_WAIT_ANY"] / wc, a["SQ_WAIT_INST_ANY"] / wc, a["SQ_ACTIVE_INST_ANY"] / wc,
+            a["SQ_ACTIVE_INST_VALU"] / wc, a["SQ_ACTIVE_INST_LDS"] / wc, a["SQ_ACTIVE_INST_VMEM"] / wc))
+    with open(out_md, "w") as f:
+        f.write("# Wave states per GEMM of the bench step (rocprofv3 counters)\n\n")
+        f.write("Command (from the repository root on an MI355X, after `cd /tmp && export TMPDIR=/tmp`):\n\n")
+        f.write("```\n%s\n```\n\n" % command)
+        f.write("Then `python bench.py --ingest-waits <counter_collection.csv>` (CPU). %d repetitions of the step's "
+                "launch sequence; means per GEMM kernel launch (the split-K reduction pass is not included). Every "
+                "column after the duration is a counter over SQ_WAVE_CYCLES, the summed lifetime of the launch's "
+                "waves:\n\n"
+                "* waiting on a dependency = SQ_WAIT_ANY (a wait count or a barrier: memory latency, LDS, or other "
+                "waves);\n"
+                "* ready, not issued = SQ_WAIT_INST_ANY (an instruction is ready but its unit or the issue port is "
+                "busy, e.g. the matrix unit running the other wave's instructions);\n"
+                "* issuing = SQ_ACTIVE_INST_ANY, split into VALU (matrix instructions included), LDS and "
+                "VMEM.\n\n" % reps)
+        f.write("\n".join(lines) + "\n")
+    return reps
+
+
+def ingest_mfma(csv_path, points, out_md, command):
+    """Matrix-core utilisation per GEMM of the step from one rocprofv3 --pmc
+    run of MFMA_COUNTERS over this script (--steps 1 --warmup 0): busy cycles
+    of the matrix units over the GPU's active cycles times the SIMDs (the
+    profiler's MfmaUtil), the matrix operations issued against the GEMM's
+    algorithmic flops, the vector-ALU instructions against those of one
+    dequantization of every weight, the LDS instruction and bank-conflict
+    counts, and the achieved clock of the longer launches."""
+    reps, acc, copies = gemm_counters(csv_path, points, MFMA_COUNTERS)
+    # GRBM_GUI_ACTIVE covers a window a fixed number of cycles longer than the
+    # dispatch: fit cycles per XCD = clock x duration + window over the copy
+    # kernels of the run (lightly loaded, so one clock) and take the window out
+    window = 0.0
+    if len(copies) >= 3:
+        cd = np.array(copies, dtype=np.float64)
+        _, window = np.polyfit(cd[:, 0], cd[:, 1] / MI355X_XCDS, 1)
     lines = ["| cfg | shape | K | N | M | kernel | matrix busy % | matrix flops / algorithmic | VALU / one dequant | "
              "clock GHz | LDS instr | LDS bank conflicts |",
              "|---|---|---|---|---|---|---|---|---|---|---|---|"]
@@ -779,6 +825,9 @@ def main():
                     help="only measure direct-to-register vs LDS write-back of the dequantized weights")
     ap.add_argument("--ablation-only", default="", metavar="K,N,M",
                     help="with --ablation: one shape, 5 launches per mode (for counter runs)")
+    ap.add_argument("--ingest-waits", metavar="COUNTER_CSV",
+                    help="write the wave-state table (profiles/wave_states_*.md) from a rocprofv3 --pmc CSV of "
+                         "WAIT_COUNTERS over --steps 1 --warmup 0")
     ap.add_argument("--ingest-mfma", metavar="COUNTER_CSV",
                     help="per-GEMM matrix-core utilisation from a rocprofv3 --pmc run of MFMA_COUNTERS")
     ap.add_argument("--mfma-out", default=os.path.join(ROOT, "profiles", "mfma_util_bench_llama2_7b_70b.md"))
@@ -808,6 +857,17 @@ def main():
         print("dominant %s mean kernel duration %.2f us" % (
             args.dominant, ingest_trace(args.ingest_trace, points, args.dominant, args.trace_out, args.trace_command,
                                         args.trace_log)))
+        return
+
+    if args.ingest_waits:
+        import paper_2402_10076_amd as Q
+        points = build_points([int(c) for c in args.configs.split(",") if c])
+        for p in points:
+            p["sel"] = Q.select_config(p["M"], p["N"], p["K"])
+            p["kernel"] = kernel_name(p["sel"])
+        cmd = ("rocprofv3 --pmc " + " ".join(WAIT_COUNTERS) + " --output-format csv -d <dir> -o sq "
+               "-- python3 <repo>/bench.py --steps 1 --warmup 0 --no-cpu-baseline")
+        print("%d repetitions ingested into %s" % (ingest_waits(args.ingest_waits, points, WAITS_MD, cmd), WAITS_MD))
         return
 
     if args.ingest_mfma:
