@@ -249,7 +249,7 @@ def test_caller_workspace_and_side_stream():
     y_int = from_dev_y(p.gemm(xd, cfg=cfg))
     need = Q.workspace_bytes(M, N, K, cfg)
     assert need > 0
-    ws = torch.empty(need // 4, dtype=torch.float32, device="cuda")
+    ws = torch.zeros(need // 4, dtype=torch.float32, device="cuda")  # arrival counters start at zero
     side = torch.cuda.Stream()
     with torch.cuda.stream(side):
         y_ws = p.gemm(xd, cfg=cfg, workspace=ws, stream=side)

@@ -38,14 +38,31 @@ def _owner(u, W, U):
     return ((u + 1) * W - 1) // U
 
 
+def streamk_dp_tiles(tiles, KG, G):
+    """Tiles the stream-K schedule runs whole, one per workgroup, before it
+    splits the rest: the whole rounds, less one when the remainder would
+    give each workgroup under half a tile (or under one k-group)."""
+    tdp = tiles // G * G
+    if 0 < tdp < tiles and (2 * (tiles - tdp) < G or (tiles - tdp) * KG < G):
+        tdp -= G
+    return tdp
+
+
 def streamk_partition(tiles, KG, G):
     """Stream-K of the tiled kernel: G workgroups (8 <= G <= tiles*KG, a
-    multiple of 8) split tiles x KG units; returns per tile the contributor
-    list [(workgroup, slot, kb, ke)] in k order."""
-    U = tiles * KG
+    multiple of 8) first run tiles wid, wid + G, .. below streamk_dp_tiles
+    whole, then split the remaining tiles x KG units; returns per tile the
+    contributor list [(workgroup, slot, kb, ke)] in k order, and the first
+    unit and the unit count of the split part."""
+    tdp = streamk_dp_tiles(tiles, KG, G)
     pieces = {}
     for wid in range(G):
-        u0, u1 = wid * U // G, (wid + 1) * U // G
+        for t in range(wid, tdp, G):
+            pieces.setdefault(t, []).append((wid, None, 0, KG))
+    ub = tdp * KG
+    U = tiles * KG - ub
+    for wid in range(G if U else 0):   # whole rounds only: nothing is split
+        u0, u1 = ub + wid * U // G, ub + (wid + 1) * U // G
         assert u1 > u0, "empty range"
         u = u0
         while u < u1:
@@ -58,27 +75,42 @@ def streamk_partition(tiles, KG, G):
             else:
                 pieces.setdefault(tt, []).append((wid, None, 0, KG))
             u += ke - kb
-    return pieces, U
+    return pieces, ub, U
 
 
 @pytest.mark.parametrize("tiles,KG,G", [(1, 32, 8), (3, 7, 16), (40, 64, 256), (256, 224, 256), (320, 64, 256),
-                                         (17, 9, 152), (5, 200, 1000)])
+                                         (17, 9, 152), (5, 200, 1000), (896, 64, 256), (36, 8, 16), (40, 8, 16),
+                                         (60, 8, 16), (16, 8, 16), (25, 3, 24), (1792, 64, 256), (300, 1, 256)])
 def test_streamk_contributors_and_slots(tiles, KG, G):
     G = min(G, tiles * KG) // 8 * 8
-    pieces, U = streamk_partition(tiles, KG, G)
+    pieces, ub, U = streamk_partition(tiles, KG, G)
     assert sorted(pieces) == list(range(tiles))
+    tdp = streamk_dp_tiles(tiles, KG, G)
+    assert tdp % G == 0 and 0 <= tdp <= tiles
+    if tdp < tiles:
+        # the split part gives every workgroup at least one k-group and,
+        # after whole rounds, between half a tile and 3/2 tiles
+        assert U >= G
+        if tdp:
+            assert G <= 2 * (tiles - tdp) < 3 * G
     for t, ps in pieces.items():
         # the k-ranges of a tile's pieces tile [0, KG) in contributor order
         assert [p[2] for p in ps][0] == 0 and ps[-1][3] == KG
         assert all(a[3] == b[2] for a, b in zip(ps, ps[1:]))
+        if t < tdp:
+            assert ps == [(t % G, None, 0, KG)]
         if len(ps) == 1:
             continue
-        tb = t * KG
+        tb = t * KG - ub
         w0, w1 = _owner(tb, G, U), _owner(tb + KG - 1, G, U)
         assert [p[0] for p in ps] == list(range(w0, w1 + 1)), "contributors are consecutive"
         for wid, slot, _, _ in ps:
             # the reader's rule for a contributor's slot
             assert slot == 2 * wid + (0 if wid * U // G >= tb else 1)
+    # one arrival counter per workgroup: the owner of a split tile's last
+    # unit owns no other split tile's last unit
+    lasts = [_owner(t * KG - ub + KG - 1, G, U) for t, ps in pieces.items() if len(ps) > 1]
+    assert len(lasts) == len(set(lasts)) and all(0 <= w < G for w in lasts)
 
 
 def grouped_tiles(offsets, R, BM, nn, part=0, unit=128, keep=64):
