@@ -124,7 +124,8 @@ int quick_w4a16_gemm(const void* x, const void* packed, const void* scales,
 typedef struct quick_config {
     int variant;   /* 0 auto, 1 = stream kernel (small M), 2 = tiled kernel,
                       3 = tiled kernel with the stream-K schedule (resident
-                      workgroups share the tiles x k-groups work equally),
+                      workgroups run the whole rounds of tiles, then share
+                      the remaining tiles x k-groups work equally),
                       4 = reserved (rejected with INVALID_ARG),
                       5 = sliced stream kernel (M <= 16: the 8 waves of a
                       workgroup split 128 or 256 columns, workgroups split

@@ -54,7 +54,7 @@ VARIANT_STREAMK32 = 7
 # CPU tests of the argument checks substitute "meta")
 _DEVICE_TYPE = "cuda"
 
-# leading workspace bytes that hold stream-K arrival counters (QUICK_WORKSPACE_COUNTER_BYTES)
+# leading workspace bytes that hold arrival counters (stream-K, sliced) (QUICK_WORKSPACE_COUNTER_BYTES)
 WS_COUNTER_BYTES = 16384
 # bytes of the per-GPU scratch array of quick_w4a16_gemm_noalloc (QUICK_SCRATCH_BYTES)
 SCRATCH_BYTES = 80 << 20
