@@ -143,9 +143,9 @@ typedef struct quick_config {
     int tile_m;    /* tiled kernel rows per workgroup: 16, 32, 64 or 128
                       (variant 5: must be 0);
                       supported (tile_m, tile_n) pairs, variants 2, 3:
-                      (16|32|64|128, 16|32), (64, 64); variants 6, 7:
+                      (16|32|64|128, 16|32); variants 6, 7:
                       (32|64|128, 32)                                        */
-    int tile_n;    /* tiled kernel columns per wave: 16, 32 or 64
+    int tile_n;    /* tiled kernel columns per wave: 16 or 32
                       stream kernels (variants 1, 5): n-tiles per wave: 1 or
                       2                                                      */
 } quick_config_t;

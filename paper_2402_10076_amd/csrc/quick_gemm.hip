@@ -1811,7 +1811,6 @@ int tiled_resident(int bm, int wn, bool mfma32)
     else if (bm == 64 && wn == 16) per = resident_per_cu(&tiled_kernel<64, 16>);
     else if (bm == 64 && wn == 32) per = resident_per_cu(&tiled_kernel<64, 32>);
     else if (bm == 128 && wn == 16) per = resident_per_cu(&tiled_kernel<128, 16>);
-    else if (bm == 64 && wn == 64) per = resident_per_cu(&tiled_kernel<64, 64>);
     else if (bm == 128 && wn == 32) per = resident_per_cu(&tiled_kernel<128, 32>);
     (void)hipGetLastError();
     const int g = std::min(cus * per, kSkMaxWorkgroups);
@@ -1885,8 +1884,7 @@ int auto_plan(int64_t M, int64_t N, int64_t K, Plan* pl)
         // Mid M with a short or medium K, when the 128 x 256 tiles are too
         // few to fill the chip: 16-column waves on 128- or 64-row tiles
         // (twice the workgroups of 32-column waves, each weight dequantized
-        // ceil(M / BM) times, and two workgroups per compute unit) when they
-        // fill it without splitting K.
+        // ceil(M / BM) times) when they fill it without splitting K.
         bool mid = false;
         if ((int64_t)ceil_div(M, 128) * ceil_div(N, 256) < 160 && KG < 128)
             for (int bm : {128, 64})
@@ -1973,8 +1971,7 @@ bool tiled32_supported(int bm, int wn)
 
 bool tiled_supported(int bm, int wn)
 {
-    return ((bm == 16 || bm == 32) && (wn == 16 || wn == 32)) || ((bm == 64 || bm == 128) && (wn == 16 || wn == 32)) ||
-           (bm == 64 && wn == 64);
+    return (bm == 16 || bm == 32 || bm == 64 || bm == 128) && (wn == 16 || wn == 32);
 }
 
 int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* pl)
@@ -2038,7 +2035,7 @@ int make_plan(int64_t M, int64_t N, int64_t K, const quick_config_t* cfg, Plan* 
             pl->bm = cfg->tile_m;
         }
         if (cfg->tile_n) {
-            if (cfg->tile_n != 16 && cfg->tile_n != 32 && cfg->tile_n != 64) return QUICK_ERR_INVALID_ARG;
+            if (cfg->tile_n != 16 && cfg->tile_n != 32) return QUICK_ERR_INVALID_ARG;
             pl->wn = cfg->tile_n;
         }
         if (cfg->split_k && !is_streamk(pl->variant)) {
@@ -2319,7 +2316,6 @@ int launch_tiled(const Plan& pl, const uint16_t* x, const u4_t* pw, const uint16
             launch_tiled_t<128, 16, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
         else if (pl.bm == 128 && pl.wn == 32)
             launch_tiled_t<128, 32, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
-        else if (pl.bm == 64 && pl.wn == 64) launch_tiled_t<64, 64, false>(pl, x, pw, ps, pz, y, ws, M, N, K, st, none, epi);
         else return QUICK_ERR_INVALID_ARG;
     }
     if (pl.variant == kVariantTiled && pl.split > 1) {
@@ -2641,8 +2637,8 @@ std::vector<quick_config_t> tune_candidates(int64_t M, int64_t N, int64_t K)
     }
     int64_t mcap = 16;
     while (mcap < M && mcap < 128) mcap *= 2;
-    static const int tiles[][2] = {{16, 16}, {16, 32}, {32, 16}, {32, 32}, {64, 16}, {64, 32}, {64, 64},
-                                   {128, 16}, {128, 32}};
+    static const int tiles[][2] = {{16, 16}, {16, 32}, {32, 16}, {32, 32}, {64, 16}, {64, 32}, {128, 16},
+                                   {128, 32}};
     for (const auto& t : tiles) {
         if (t[0] > mcap) continue;
         for (int s : {1, 2, 4, 8})

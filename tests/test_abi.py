@@ -162,6 +162,7 @@ def test_gemm_ex_validation_without_device():
     assert ex(Q.make_config(variant=2, split_k=33)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=2, tile_m=256, tile_n=64)) == Q.QUICK_ERR_INVALID_ARG
     assert ex(Q.make_config(variant=2, tile_m=128, tile_n=64)) == Q.QUICK_ERR_INVALID_ARG
+    assert ex(Q.make_config(variant=2, tile_m=64, tile_n=64)) == Q.QUICK_ERR_INVALID_ARG   # withdrawn: it spilled
     cfg = Q.make_config(variant=2, tile_m=128, tile_n=32, split_k=4)
     need = Q.workspace_bytes(256, 4096, 4096, cfg)
     assert need == Q.WS_COUNTER_BYTES + 4 * 256 * 4096 * 4

@@ -37,7 +37,6 @@ CFGS = [None,
         dict(variant=1, split_k=1, tile_n=2), dict(variant=1, split_k=4, tile_n=2),
         dict(variant=2, split_k=1, tile_m=16, tile_n=32), dict(variant=2, split_k=1, tile_m=64, tile_n=32),
         dict(variant=2, split_k=3, tile_m=32, tile_n=16), dict(variant=2, split_k=2, tile_m=128, tile_n=32),
-        dict(variant=2, split_k=1, tile_m=64, tile_n=64),
         dict(variant=3, split_k=24, tile_m=32, tile_n=32), dict(variant=3, split_k=16, tile_m=128, tile_n=32),
         dict(variant=6, split_k=1, tile_m=64, tile_n=32), dict(variant=6, split_k=3, tile_m=32, tile_n=32),
         dict(variant=7, split_k=16, tile_m=128, tile_n=32)]
