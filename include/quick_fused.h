@@ -44,8 +44,8 @@ typedef struct quick_epilogue {
  * (SHAPE otherwise) and y is M x N/2.  The gated form needs each gate tile
  * and its up tile in one wave: an automatic configuration is adjusted for
  * it; an explicit cfg that cannot hold them (stream kernel with one n-tile
- * per wave, tiled kernel with 16-column waves and no K split) or the
- * balanced stream kernel (variant 4) with any epilogue is INVALID_ARG.
+ * per wave, tiled kernel with 16-column waves and no K split) is
+ * INVALID_ARG, as is the reserved variant 4.
  * The workspace a caller passes must hold quick_fused_workspace_bytes().
  * Other arguments, errors and the workspace contract as quick_w4a16_gemm_ex;
  * also INVALID_ARG for an unknown activation, ALIGNMENT for the bias. */

@@ -1965,7 +1965,7 @@ bool tuned_config(int64_t M, int64_t N, int64_t K, quick_config_t* out)
 
 bool tiled32_supported(int bm, int wn)
 {
-    // (64 x 64 wave tiles spill registers in this form)
+    // (64 x 64 wave tiles spill registers)
     return (bm == 32 || bm == 64 || bm == 128) && wn == 32;
 }
 
@@ -2604,10 +2604,10 @@ extern "C" int quick_select_config(int64_t M, int64_t N, int64_t K, quick_config
 
 namespace {
 
-// Configurations worth timing for a shape: the balanced stream kernel (M <=
-// 16 with x fitting in LDS), the stream kernel (small M), the sliced stream
-// kernel (M <= 16), the tiled tiles no taller than the next power of two >= M (at least 16) with
-// splits 1, 2, 4, 8 (each slice keeping >= 2 k-groups), and stream-K.
+// Configurations worth timing for a shape: the stream kernel (small M), the
+// sliced stream kernel (M <= 16), the tiled tiles no taller than the next
+// power of two >= M (at least 16) with splits 1, 2, 4, 8 (each slice keeping
+// >= 2 k-groups), and stream-K.
 std::vector<quick_config_t> tune_candidates(int64_t M, int64_t N, int64_t K)
 {
     std::vector<quick_config_t> c;

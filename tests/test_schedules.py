@@ -5,9 +5,10 @@
   workspace the automatic path reports equals the one of that explicit
   configuration.
 * The index arithmetic of the persistent schedules, written out the way the
-  kernels compute it: the stream-K split of tiles x k-groups, the grouped
-  form's per-expert tile table, and the balanced stream kernel's trip-aligned
-  ranges.  Each must cover every unit exactly once, give every shared tile a
+  kernels compute it: the stream-K schedule (whole rounds of tiles, then the
+  rest of tiles x k-groups split), the grouped form's per-expert tile table,
+  and the sliced stream kernel's slices.  Each must cover every unit exactly
+  once, give every shared tile a
   contiguous run of contributors whose partial-slot indices agree between
   writer and reader, and keep every access inside its buffer.  (These are the
   checks run before each schedule first ran on a GPU.)
