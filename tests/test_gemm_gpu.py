@@ -127,6 +127,42 @@ def test_streamk_rounds_then_pieces(rounds, variant, wn):
     _check(M, 1024, N, dict(variant=variant, tile_m=bm, tile_n=wn, split_k=G), seed=int(rounds * 100) + variant)
 
 
+@pytest.mark.parametrize("K,N", [(128, 16), (128, 272), (256, 16), (128, 4112)])
+@pytest.mark.parametrize("M", [1, 17, 200])
+def test_smallest_k_and_n(M, K, N):
+    """One k-group and one n-tile, the edges of the tile space: every
+    configuration that accepts the shape (stream, tiled and its split and
+    stream-K schedules on both matrix instructions, sliced) matches the
+    oracle element by element.  A split-K request above K / 128 slices is
+    INVALID_ARG; stream-K on fewer than 8 tiles x k-groups runs whole
+    tiles."""
+    x, q, z, s = rand_case(M * 7 + K + N, M, K, N)
+    p = Packed(q, z, s)
+    xd = to_dev_x(x)
+    ref = oracle.gemm(x, q, z, s)
+    cfgs = [None] + [dict(variant=1, split_k=w, tile_n=n) for w in (1, 8) for n in (1, 2)] + \
+        [dict(variant=v, tile_m=bm, tile_n=wn, split_k=sk) for v, sk in ((2, 1), (2, 2), (3, 0), (3, 8))
+         for bm, wn in ((16, 16), (32, 32), (128, 32))] + \
+        [dict(variant=v, tile_m=64, tile_n=32, split_k=sk) for v, sk in ((6, 1), (6, 2), (7, 0))] + \
+        [dict(variant=5, split_k=0, tile_n=n) for n in (1, 2)]
+    ran = 0
+    for c in cfgs:
+        if c and c["variant"] == 1 and M > 64:
+            continue
+        if c and c["variant"] == 5 and M > 16:
+            continue
+        if c and c["variant"] in (2, 6) and c["split_k"] > K // 128:
+            with pytest.raises(Q.QuickError) as e:
+                p.gemm(xd, cfg=Q.make_config(**c))
+            assert e.value.status == Q.QUICK_ERR_INVALID_ARG
+            continue
+        say("smallest K=%d N=%d M=%d cfg=%s" % (K, N, M, c))
+        y = from_dev_y(p.gemm(xd, cfg=Q.make_config(**c) if c else None))
+        assert rel_err(y, ref) <= TOL, c
+        ran += 1
+    assert ran >= 12
+
+
 @pytest.mark.parametrize("M", [1, 2, 5, 16, 31, 64, 65, 96, 127, 200, 513])
 def test_auto_config_small_shapes(M):
     _check(M, 1024, 272, None, seed=M)
