@@ -1,0 +1,58 @@
+"""Seeded random shapes under random explicit configurations: every kernel,
+tile, split and schedule the library accepts, on shapes with ragged M and
+N tails, checked element by element against the oracle.  A configuration
+the library rejects must be rejected with INVALID_ARG and is counted."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2402_10076_amd as Q
+from gpu_util import TOL, Packed, from_dev_y, rand_case, rel_err, say, to_dev_x
+
+pytestmark = pytest.mark.gpu
+
+TILES = ((16, 16), (16, 32), (32, 16), (32, 32), (64, 16), (64, 32), (128, 16), (128, 32))
+TILES32 = ((32, 32), (64, 32), (128, 32))
+
+
+def _random_cfg(g, M, K):
+    v = int(g.choice([0, 1, 2, 3, 5, 6, 7]))
+    if v == 0:
+        return None
+    if v == 1:
+        return dict(variant=1, split_k=int(g.choice([1, 2, 4, 8])), tile_n=int(g.choice([1, 2])))
+    if v == 5:
+        return dict(variant=5, split_k=int(g.integers(0, K // 128 + 1)), tile_n=int(g.choice([1, 2])))
+    bm, wn = (TILES32 if v in (6, 7) else TILES)[int(g.integers(0, len(TILES32 if v in (6, 7) else TILES)))]
+    if v in (3, 7):
+        sk = int(g.choice([0, 8, 16, 24, 64, 256]))
+    else:
+        sk = int(g.integers(1, min(8, K // 128) + 1))
+    return dict(variant=v, tile_m=bm, tile_n=wn, split_k=sk)
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_random_shapes_and_configs(seed):
+    g = np.random.Generator(np.random.PCG64(9000 + seed))
+    ran = rejected = 0
+    for case in range(20):
+        M = int(g.choice([1, 2, 3, 7, 16, 17, 33, 64, 65, 100, 128, 129]))
+        K = 128 * int(g.integers(1, 17))
+        N = 16 * int(g.integers(1, 65))
+        x, q, z, s = rand_case(int(g.integers(1 << 30)), M, K, N)
+        p = Packed(q, z, s)
+        xd = to_dev_x(x)
+        ref = oracle.gemm(x, q, z, s)
+        for _ in range(3):
+            cfg = _random_cfg(g, M, K)
+            say("random seed=%d case=%d M=%d K=%d N=%d cfg=%s" % (seed, case, M, K, N, cfg))
+            try:
+                y = from_dev_y(p.gemm(xd, cfg=Q.make_config(**cfg) if cfg else None))
+            except Q.QuickError as e:
+                assert e.status == Q.QUICK_ERR_INVALID_ARG, (cfg, e)
+                rejected += 1
+                continue
+            assert rel_err(y, ref) <= TOL, (M, K, N, cfg)
+            ran += 1
+    say("random seed=%d: %d runs, %d rejected configurations" % (seed, ran, rejected))
+    assert ran >= 40
