@@ -56,3 +56,43 @@ def test_random_shapes_and_configs(seed):
             ran += 1
     say("random seed=%d: %d runs, %d rejected configurations" % (seed, ran, rejected))
     assert ran >= 40
+
+
+GROUPED_TILES = ((16, 16), (16, 32), (32, 16), (32, 32), (64, 32), (128, 32))
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_random_grouped(seed):
+    """The grouped form on random expert counts (empty experts and one-row
+    experts included), random token routing and random explicit
+    configurations, against the oracle's grouped GEMM."""
+    from test_grouped_gpu import Grouped, _experts, _routing
+    g = np.random.Generator(np.random.PCG64(7000 + seed))
+    ran = 0
+    for case in range(6):
+        E = int(g.integers(1, 9))
+        K = 128 * int(g.integers(1, 9))
+        N = 16 * int(g.integers(1, 33))
+        T = int(g.integers(1, 200))
+        counts = [int(c) for c in g.choice([0, 1, 2, 15, 16, 17, 63, 64, 65, 127, 128, 129, 150], size=E)]
+        rows, offsets = _routing(int(g.integers(1 << 30)), T, E, counts=counts)
+        experts = _experts(int(g.integers(1 << 30)), E, K, N)
+        x = rand_case(int(g.integers(1 << 30)), T, K, 16)[0]
+        ref = oracle.grouped_gemm(x, rows, offsets, experts)
+        gp = Grouped(experts)
+        xd = to_dev_x(x)
+        for _ in range(3):
+            v = int(g.choice([0, 2, 3]))
+            if v == 0:
+                cfg = None
+            else:
+                bm, wn = GROUPED_TILES[int(g.integers(0, len(GROUPED_TILES)))]
+                sk = int(g.integers(1, min(4, K // 128) + 1)) if v == 2 else int(g.choice([0, 8, 64]))
+                cfg = dict(variant=v, tile_m=bm, tile_n=wn, split_k=sk)
+            say("random grouped seed=%d case=%d E=%d T=%d K=%d N=%d counts=%s cfg=%s" % (
+                seed, case, E, T, K, N, counts, cfg))
+            y = from_dev_y(gp.run(xd, rows, offsets, cfg=Q.make_config(**cfg) if cfg else None))
+            if offsets[-1]:
+                assert rel_err(y, ref) <= TOL, (E, counts, cfg)
+            ran += 1
+    assert ran == 18
