@@ -1,4 +1,5 @@
-"""Seeded random shapes under random explicit configurations: every kernel,
+"""Seeded random shapes under random explicit configurations (plain, grouped
+and fused-epilogue forms): every kernel,
 tile, split and schedule the library accepts, on shapes with ragged M and
 N tails, checked element by element against the oracle.  A configuration
 the library rejects must be rejected with INVALID_ARG and is counted."""
@@ -96,3 +97,42 @@ def test_random_grouped(seed):
                 assert rel_err(y, ref) <= TOL, (E, counts, cfg)
             ran += 1
     assert ran == 18
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_fused_epilogues(seed):
+    """Bias and the gated SiLU on random shapes and random explicit
+    configurations, against the oracle's GEMM and binary64 epilogue; a
+    configuration that cannot pair gate and up tiles in one wave is
+    INVALID_ARG."""
+    from test_fused_gpu import _bias, _dev_bias, _gate_up
+    g = np.random.Generator(np.random.PCG64(5000 + seed))
+    ran = 0
+    for case in range(8):
+        M = int(g.choice([1, 5, 16, 17, 64, 65, 130]))
+        K = 128 * int(g.integers(1, 13))
+        Nh = 16 * int(g.integers(1, 33))
+        act = int(g.integers(0, 2))
+        if act:
+            q, z, s = _gate_up(int(g.integers(1 << 30)), K, Nh)
+        else:
+            _, q, z, s = rand_case(int(g.integers(1 << 30)), 1, K, Nh)
+        N = q.shape[1]
+        x = rand_case(int(g.integers(1 << 30)), M, K, 16)[0]
+        b = _bias(int(g.integers(1 << 30)), N)
+        dw, ds, dz = Q.to_device(*Q.pack_weights(q, z, s))
+        ref = oracle.epilogue(oracle.gemm(x, q, z, s), b, act=act)
+        xd = to_dev_x(x)
+        for _ in range(3):
+            cfg = _random_cfg(g, M, K)
+            say("random fused seed=%d case=%d M=%d K=%d N=%d act=%d cfg=%s" % (seed, case, M, K, N, act, cfg))
+            try:
+                y = from_dev_y(Q.gemm_fused(xd, dw, ds, dz, N, bias=_dev_bias(b), activation=act,
+                                            cfg=Q.make_config(**cfg) if cfg else None))
+            except Q.QuickError as e:
+                assert e.status == Q.QUICK_ERR_INVALID_ARG, (cfg, e)
+                continue
+            assert y.shape == (M, N // 2 if act else N)
+            assert rel_err(y, ref) <= TOL, (M, K, N, act, cfg)
+            ran += 1
+    assert ran >= 10
