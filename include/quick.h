@@ -21,6 +21,10 @@
  *    patterns stored in uint16_t.
  *  - Only group == 128 is supported (QUICK_ERR_UNSUPPORTED otherwise);
  *    K must be a multiple of 128 and N a multiple of 16 (QUICK_ERR_SHAPE).
+ *  - 32-bit limits (the kernels address their buffers with 32-bit offsets):
+ *    packed weights K*N/2 < 2^32 bytes, M*K < 2^31 activation elements,
+ *    M*N < 2^31 output elements and M <= 2^24; larger shapes are
+ *    QUICK_ERR_SHAPE.
  */
 #ifndef QUICK_H
 #define QUICK_H
@@ -35,7 +39,8 @@ extern "C" {
 /* ---- status codes ---------------------------------------------------- */
 #define QUICK_OK 0
 #define QUICK_ERR_INVALID_ARG 1  /* null pointer, bad config field          */
-#define QUICK_ERR_SHAPE 2        /* M < 0, K % 128, N % 16, K or N <= 0     */
+#define QUICK_ERR_SHAPE 2        /* M < 0, K % 128, N % 16, K or N <= 0,
+                                    a 32-bit limit exceeded                  */
 #define QUICK_ERR_UNSUPPORTED 3  /* group != 128                             */
 #define QUICK_ERR_RANGE 4        /* a q or z value above 15                  */
 #define QUICK_ERR_ALIGNMENT 5    /* device pointer not aligned (see below)   */

@@ -69,3 +69,21 @@ def rand_case(seed, M, K, N, outliers=False):
     z = g.integers(0, 16, (K // 128, N), dtype=np.uint8)
     s = g.uniform(0.002, 0.02, (K // 128, N)).astype(np.float16).view(np.uint16)
     return x, q, z, s
+
+
+def decode_qpk16_tile(pw_words: np.ndarray, pz_words: np.ndarray, ps_halves: np.ndarray, K: int):
+    """(q [K][16], z [K/128][16], s bits [K/128][16]) of one n-tile from its
+    QPK16 words: the tile's K/128 units of 64 lanes x 4 words (lane 16g + c,
+    word j holds channels 32j + 8g + e of column c, element e in nibble slot
+    e/2 + 4(e%2)), its 2 zero words per k-group (column c in nibble c%8 of
+    word c/8) and its 16 scale halves per k-group.  Test infrastructure: the
+    tests check it against the oracle's pack, which defines the layout."""
+    KG = K // 128
+    w = np.asarray(pw_words, np.uint32).reshape(KG, 4, 16, 4)          # kg, g, c, j
+    q = np.empty((KG, 4, 4, 8, 16), np.uint8)                           # kg, j, g, e, c
+    for slot in range(8):
+        e = 2 * (slot % 4) + slot // 4
+        q[:, :, :, e, :] = ((w >> np.uint32(4 * slot)) & np.uint32(15)).transpose(0, 3, 1, 2)
+    zw = np.asarray(pz_words, np.uint32).reshape(KG, 2, 1)
+    z = ((zw >> (4 * np.arange(8, dtype=np.uint32))) & np.uint32(15)).reshape(KG, 16).astype(np.uint8)
+    return q.reshape(K, 16), z, np.asarray(ps_halves, np.uint16).reshape(KG, 16).copy()

@@ -95,8 +95,13 @@ def test_gemm_validation_without_device():
     assert _gemm(A, A, A + 1, A, A, 4, 4096, 4096) == Q.QUICK_ERR_ALIGNMENT
     assert _gemm(A, A, A, A + 2, A, 4, 4096, 4096) == Q.QUICK_ERR_ALIGNMENT
     assert _gemm(A, A, A, A, A + 4, 4, 4096, 4096) == Q.QUICK_ERR_ALIGNMENT
-    # 32-bit index limits
+    # 32-bit index limits: each at its first rejected value (the largest
+    # accepted ones run on the GPU in test_limits_gpu.py)
     assert _gemm(**ok, M=4, N=1 << 20, K=1 << 17) == Q.QUICK_ERR_SHAPE
+    assert _gemm(**ok, M=4, N=131072, K=65536) == Q.QUICK_ERR_SHAPE          # K*N/2 == 2^32 bytes
+    assert _gemm(**ok, M=1 << 19, N=48, K=4096) == Q.QUICK_ERR_SHAPE         # M*K == 2^31
+    assert _gemm(**ok, M=1 << 16, N=32768, K=128) == Q.QUICK_ERR_SHAPE       # M*N == 2^31
+    assert _gemm(**ok, M=(1 << 24) + 1, N=16, K=128) == Q.QUICK_ERR_SHAPE    # M > 2^24
 
 
 def test_noalloc_validation_without_device(tmp_path):

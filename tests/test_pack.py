@@ -98,3 +98,18 @@ def test_interleave_gate_up_matches_oracle_layout():
     q, z, s = Q.interleave_gate_up(gate, up)
     for got, a, b in zip((q, z, s), gate, up):
         assert np.array_equal(got, oracle.interleave_gate_up(a, b))
+
+
+def test_tile_decode_inverts_oracle_pack():
+    """The tests' decoder of one n-tile's QPK16 words (used where inputs are
+    drawn on the device in packed form) against the oracle's definition."""
+    from gpu_util import decode_qpk16_tile
+    K, N = 512, 64
+    q, z, s = _weights(99, K, N)
+    ow, oz, os_ = oracle.pack(q, z, s)
+    KG = K // 128
+    for nt in range(N // 16):
+        dq, dz, ds = decode_qpk16_tile(ow[nt * KG * 256:(nt + 1) * KG * 256], oz[nt * KG * 2:(nt + 1) * KG * 2],
+                                       os_[nt * KG * 16:(nt + 1) * KG * 16], K)
+        cols = slice(16 * nt, 16 * nt + 16)
+        assert np.array_equal(dq, q[:, cols]) and np.array_equal(dz, z[:, cols]) and np.array_equal(ds, s[:, cols])
