@@ -6,7 +6,9 @@ oracle on sampled tiles or rows:
 * weights just under 4 GiB (K = 65536, N = 131056): every unit offset of the
   last n-tiles sits just below 2^32 bytes;
 * activations just under 2^31 elements (M = 524287 rows of K = 4096);
-* outputs just under 2^31 elements (M = 65535 rows of N = 32752).
+* outputs just under 2^31 elements (M = 65535 rows of N = 32752);
+* the grouped form over 8 experts of 1 GiB each, whose buffers start beyond
+  2^32 bytes.
 
 Inputs of this size are drawn on the device with a seeded torch generator:
 x as normal f16, the packed weights and zero points as uniform random bytes
@@ -32,10 +34,11 @@ def _gen(seed):
     return g
 
 
-def _dev_weights(seed, K, N):
-    """Random packed weights, zero points and scales of a K x N matrix, on the device."""
+def _dev_weights(seed, K, N, experts=1):
+    """Random packed weights, zero points and scales of `experts` K x N
+    matrices back to back, on the device."""
     g = _gen(seed)
-    wb, zb, sb = Q.packed_sizes(K, N)   # packed, zero-point and scale bytes
+    wb, zb, sb = (experts * b for b in Q.packed_sizes(K, N))   # packed, zero-point and scale bytes
     pw = torch.randint(0, 256, (wb,), dtype=torch.uint8, device="cuda", generator=g).view(torch.int32)
     pz = torch.randint(0, 256, (zb,), dtype=torch.uint8, device="cuda", generator=g).view(torch.int32)
     ps = (torch.rand(sb // 2, device="cuda", generator=g) * 0.018 + 0.002).half().view(torch.int16)
@@ -152,4 +155,46 @@ def test_largest_outputs():
         assert err <= TOL, "plan %s: %.3g" % (_cid(c), err)
         del y
     del x
+    torch.cuda.empty_cache()
+
+
+BIG_E = [None, dict(variant=2, split_k=1, tile_m=16, tile_n=16), dict(variant=2, split_k=1, tile_m=32, tile_n=32),
+         dict(variant=3, split_k=16, tile_m=64, tile_n=32), dict(variant=2, split_k=3, tile_m=16, tile_n=16)]
+
+
+def test_grouped_experts_beyond_4gib():
+    """Grouped form over 8 experts of 1 GiB of packed weights each (8 GiB
+    back to back, so the later experts' buffers start beyond 2^32 bytes),
+    gathered token rows, empty experts included."""
+    K, N, E, T = 32768, 65536, 8, 64
+    counts = [3, 0, 5, 1, 7, 2, 0, 9]
+    say("grouped, 8 x 1 GiB experts: K=%d N=%d" % (K, N))
+    pw, ps, pz = _dev_weights(41, K, N, experts=E)
+    x = torch.randn(T, K, device="cuda", generator=_gen(42), dtype=torch.float16)
+    xb = x.cpu().view(torch.int16).numpy().view(np.uint16)
+    g = np.random.Generator(np.random.PCG64(43))
+    rows = g.integers(0, T, sum(counts)).astype(np.int32)
+    offsets = np.concatenate([[0], np.cumsum(counts)]).astype(np.int32)
+    NT, KG = N // 16, K // 128
+    wb, zb, sb = Q.packed_sizes(K, N)
+    tiles = [0, NT - 1, int(g.integers(1, NT - 1))]
+    refs = {}
+    for e in range(E):
+        lo, hi = int(offsets[e]), int(offsets[e + 1])
+        if hi == lo:
+            continue
+        # expert e's buffers start wb, sb, zb bytes after expert e-1's
+        we, se, ze = pw[e * wb // 4:(e + 1) * wb // 4], ps[e * sb // 2:(e + 1) * sb // 2], pz[e * zb // 4:(e + 1) * zb // 4]
+        for nt in tiles:
+            q_t, z_t, s_t = _host_tile(we, se, ze, K, nt)
+            refs[(e, nt)] = oracle.gemm(xb[rows[lo:hi]], q_t, z_t, s_t)
+    od, rd = torch.from_numpy(offsets).cuda(), torch.from_numpy(rows).cuda()
+    for c in BIG_E:
+        say("  plan %s" % _cid(c))
+        y = from_dev_y(Q.grouped_gemm(x, od, pw, ps, pz, N, rows=rd, cfg=_cfg(c)))
+        for (e, nt), ref in refs.items():
+            lo, hi = int(offsets[e]), int(offsets[e + 1])
+            err = rel_err(y[lo:hi, 16 * nt:16 * nt + 16], ref)
+            assert err <= TOL, "plan %s, expert %d, n-tile %d: %.3g" % (_cid(c), e, nt, err)
+    del pw, ps, pz
     torch.cuda.empty_cache()
