@@ -309,6 +309,7 @@ MFMA_COUNTERS = ("SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_VALU_MFMA_MOPS_F16", "SQ_
                  "SQ_LDS_BANK_CONFLICT", "SQ_INSTS_VALU", "SQ_WAVE_CYCLES", "GRBM_GUI_ACTIVE")
 MI355X_XCDS = 8
 MI355X_SIMDS = 256 * 4
+MI355X_PEAK_GHZ = 2.4
 
 
 def gemm_counters(csv_path, points, counters):
@@ -412,8 +413,13 @@ def ingest_mfma(csv_path, points, out_md, command):
         # 32768 for the 32x32x16 form)
         mfma_insts = mflops / (32768.0 if p["kernel"].startswith("tiled32") else 16384.0)
         clock = (active - window) / a["dur"] if a["dur"] >= 20000 else float("nan")
-        lines.append("| C%d | %s | %d | %d | %d | %s | %.1f | %.2f | %.2f | %s | %.3g | %.3g |" % (
-            p["cid"], p["shape"], p["K"], p["N"], p["M"], p["kernel"], util, mflops / p["flops"],
+        if clock > MI355X_PEAK_GHZ:
+            # more than the kernel fell into the counter window: the clock
+            # (and the busy fraction over that window) is not the kernel's
+            clock, util = float("nan"), float("nan")
+        lines.append("| C%d | %s | %d | %d | %d | %s | %s | %.2f | %.2f | %s | %.3g | %.3g |" % (
+            p["cid"], p["shape"], p["K"], p["N"], p["M"], p["kernel"], "%.1f" % util if util == util else "-",
+            mflops / p["flops"],
             (a["SQ_INSTS_VALU"] - mfma_insts) / deq, "%.2f" % clock if clock == clock else "-", a["SQ_INSTS_LDS"],
             a["SQ_LDS_BANK_CONFLICT"]))
     with open(out_md, "w") as f:
@@ -434,8 +440,10 @@ def ingest_mfma(csv_path, points, out_md, command):
                 "the ideal is the number of row tiles, ceil(M / BM).\n"
                 "* clock = (GRBM_GUI_ACTIVE / %d XCDs - window) / kernel duration (counter-run timestamps), for "
                 "launches of at least 20 us; window = %.0f cycles, the fixed excess of the counter window over the "
-                "dispatch, fitted over the run's runtime copy kernels.\n\n" % (
-                    reps, MI355X_XCDS, MI355X_SIMDS, MI355X_XCDS, window))
+                "dispatch, fitted over the run's runtime copy kernels. Where this comes out above the chip's "
+                "%.1f GHz peak clock, more than the kernel fell into the counter window: that row's clock and "
+                "matrix busy %% are shown as -.\n\n" % (
+                    reps, MI355X_XCDS, MI355X_SIMDS, MI355X_XCDS, window, MI355X_PEAK_GHZ))
         f.write("\n".join(lines) + "\n")
     return reps
 

@@ -2409,8 +2409,6 @@ int validate(const void* x, const void* packed, const void* scales, const void* 
 {
     if (group != quick::kGroup) return QUICK_ERR_UNSUPPORTED;
     if (M < 0 || N <= 0 || K <= 0 || K % 128 != 0 || N % 16 != 0) return QUICK_ERR_SHAPE;
-    // 32-bit index arithmetic inside the kernels: keep every operand well
-    // inside the range (largest: packed words K*N/8, activations M*K).
     // 32-bit buffer offsets and index arithmetic inside the kernels: packed
     // weights (K*N/2 bytes) and activations (2*M*K bytes) below 4 GiB, the
     // output below 2^31 elements.
