@@ -242,15 +242,20 @@ def ingest_trace(trace_csv, points, dominant, out_md, command, run_log=""):
             if p["kernel"] == dominant:
                 dom_launch.append(rows[j][2])
             j += n
-    lines = ["| cfg | shape | K | N | M | kernel | mean us | min us | GB/s | TFLOP/s |",
-             "|---|---|---|---|---|---|---|---|---|---|"]
+    def roof_us(p):
+        # the GEMM's time at its binding roofline (HBM bytes or matrix flops at peak)
+        return max(p["bytes"] / HBM_PEAK_GBS / 1e3, p["flops"] / MFMA_F16_PEAK_TFLOPS / 1e6)
+
+    lines = ["| cfg | shape | K | N | M | kernel | mean us | min us | GB/s | TFLOP/s | bound | fraction of roofline |",
+             "|---|---|---|---|---|---|---|---|---|---|---|---|"]
     tot = 0.0
     for i, p in enumerate(points):
         mu = float(np.mean(per_point[i]))
         tot += mu
-        lines.append("| C%d | %s | %d | %d | %d | %s | %.2f | %.2f | %.0f | %.1f |" % (
+        hbm = p["bytes"] / HBM_PEAK_GBS / 1e3 >= p["flops"] / MFMA_F16_PEAK_TFLOPS / 1e6
+        lines.append("| C%d | %s | %d | %d | %d | %s | %.2f | %.2f | %.0f | %.1f | %s | %.3f |" % (
             p["cid"], p["shape"], p["K"], p["N"], p["M"], p["kernel"], mu, min(per_point[i]),
-            p["bytes"] / mu / 1e3, p["flops"] / mu / 1e6))
+            p["bytes"] / mu / 1e3, p["flops"] / mu / 1e6, "hbm" if hbm else "mfma", roof_us(p) / mu))
     dom_us = float(np.mean(dom_launch))
     # the replays of the graph of the dominant kernel's launches alone, which
     # follow the step repetitions: the launches bench.py's roofline times
@@ -263,6 +268,11 @@ def ingest_trace(trace_csv, points, dominant, out_md, command, run_log=""):
     small = [i for i, p in enumerate(points) if p["M"] <= 16]
     s_us = sum(float(np.mean(per_point[i])) for i in small)
     s_gbs = sum(points[i]["bytes"] for i in small) / s_us / 1e3
+    big = [i for i, p in enumerate(points) if p["M"] >= 256]
+    b_tf = sum(points[i]["flops"] for i in big) / sum(float(np.mean(per_point[i])) for i in big) / 1e6 if big else 0
+    band = [i for i, p in enumerate(points) if 64 <= p["M"] <= 256]
+    band_frac = (sum(roof_us(points[i]) for i in band) / sum(float(np.mean(per_point[i])) for i in band)
+                 if band else 0)
     with open(out_md, "w") as f:
         f.write("# Kernel durations of the bench step (rocprofv3 kernel trace)\n\n")
         f.write("Command (from the repository root on an MI355X, after `cd /tmp && export TMPDIR=/tmp`):\n\n")
@@ -288,7 +298,15 @@ def ingest_trace(trace_csv, points, dominant, out_md, command, run_log=""):
                     "(replay time of that graph / launches, so it also holds the gaps between launches), "
                     "`frac` = %.4f.\n" % (roof["avg_launch_us"], roof["frac"]))
         f.write("* Sum of kernel time per step: %.1f us.\n" % tot)
-        f.write("* GEMMs with M <= 16: %.1f us of kernels, %.0f GB/s of algorithmic bytes.\n\n" % (s_us, s_gbs))
+        f.write("* GEMMs with M <= 16: %.1f us of kernels, %.0f GB/s of algorithmic bytes (%.3f of %d GB/s).\n" % (
+            s_us, s_gbs, s_gbs / HBM_PEAK_GBS, HBM_PEAK_GBS))
+        if big:
+            f.write("* GEMMs with M >= 256: %.1f TFLOP/s of kernel time (%.3f of %d TFLOP/s).\n" % (
+                b_tf, b_tf / MFMA_F16_PEAK_TFLOPS, MFMA_F16_PEAK_TFLOPS))
+        if band:
+            f.write("* GEMMs with 64 <= M <= 256 (%d): %.3f of their binding rooflines together (sum of the "
+                    "roofline times over the sum of the kernel times).\n" % (len(band), band_frac))
+        f.write("\n")
         f.write("\n".join(lines) + "\n")
         stats = trace_csv.replace("_kernel_trace.csv", "_kernel_stats.csv")
         if stats != trace_csv and os.path.exists(stats):
